@@ -1,0 +1,103 @@
+"""Seeded synthetic inputs shared by the tests, the bench and the smoke check.
+
+This module draws random numbers and nothing else: it holds none of the
+quantization, matmul or normalisation arithmetic of the method, so both the
+oracle side and the HIP side can take their inputs from it without sharing
+any computation.
+
+Workload recipe (the paper's screening set is private and absent; these
+synthetic tensors stand in for it with the shapes of a 175B-wide decoder):
+  * a protein-ligand pair is 512 tokens (about 450 residue and 60 ligand
+    tokens, padded), so 4 pairs give M = 2048 rows and 8 pairs M = 4096;
+  * weights W [N, K] are N(0, 0.02) fp32 before quantization;
+  * activations x [M, K] are N(0, 1) rounded to bf16, optionally with 1 % of
+    the K channels (columns) scaled by 20 before rounding (outliers).
+
+bf16 tensors are carried as uint16 bit patterns (numpy has no bf16).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TOKENS_PER_PAIR = 512
+
+# seed bases per workload
+SEED_TOY, SEED_QKV, SEED_FFN, SEED_GEMV, SEED_STACK = 0, 1, 2, 3, 4
+
+
+def matrix_seed(workload_seed: int, layer: int, matrix_idx: int) -> int:
+    """Seed of one weight matrix: 1000*workload + 4*layer + matrix index
+    (0 = qkv, 1 = out, 2 = up, 3 = down)."""
+    return 1000 * workload_seed + 4 * layer + matrix_idx
+
+
+def _rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def f32_to_bf16_bits(z: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (round-to-nearest-even) via torch's CPU cast,
+    returned as uint16 bit patterns.  Used only to build inputs."""
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(z, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def weights_f32(seed: int, N: int, K: int, std: float = 0.02) -> np.ndarray:
+    """W [N, K] fp32 ~ N(0, std)."""
+    z = _rng(seed).standard_normal((N, K), dtype=np.float32)
+    z *= np.float32(std)
+    return z
+
+
+def activations_bf16(seed: int, M: int, K: int, outlier_frac: float = 0.0,
+                     outlier_scale: float = 20.0) -> np.ndarray:
+    """x [M, K] as bf16 bits: N(0,1); round(outlier_frac*K) distinct columns
+    scaled by outlier_scale in fp32 before the bf16 rounding."""
+    rng = _rng(seed + 7_000_000)
+    z = rng.standard_normal((M, K), dtype=np.float32)
+    n_out = int(round(outlier_frac * K))
+    if n_out:
+        cols = rng.choice(K, n_out, replace=False)
+        z[:, cols] *= np.float32(outlier_scale)
+    return f32_to_bf16_bits(z)
+
+
+def ternary_bf16(seed: int, M: int, K: int) -> np.ndarray:
+    """x [M, K] with entries in {-1, 0, +1} (exact in bf16), as bf16 bits."""
+    v = _rng(seed + 8_000_000).integers(-1, 2, size=(M, K), dtype=np.int8)
+    out = np.zeros((M, K), dtype=np.uint16)
+    out[v == 1] = 0x3F80
+    out[v == -1] = 0xBF80
+    return out
+
+
+def random_packed_bytes(seed: int, N: int, K: int) -> np.ndarray:
+    """qweight [N, K/2] of uniform random bytes: every byte holds two 4-bit
+    two's-complement codes, so uniform bytes are uniform codes in [-8, 7]."""
+    return _rng(seed + 9_000_000).integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+
+
+def const_f16_bits(N: int, G: int, bits: int) -> np.ndarray:
+    """A [N, G] array filled with one binary16 bit pattern."""
+    return np.full((N, G), bits, dtype=np.uint16)
+
+
+def residual_f32(seed: int, M: int, d: int) -> np.ndarray:
+    """Initial residual stream h0 = float32(bf16(N(0,1))) [M, d]."""
+    bits = activations_bf16(seed + 11_000_000, M, d)
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def weights_f32_cuda(seed: int, N: int, K: int, std: float = 0.02, out=None):
+    """W [N, K] fp32 ~ N(0, std) drawn on the current CUDA device with torch's
+    seeded generator (for matrices too large to stage on the host)."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.float32, device="cuda")
+    out.normal_(0.0, std, generator=g)
+    return out
