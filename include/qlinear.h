@@ -1,0 +1,212 @@
+/*
+ * qlinear.h -- C ABI of the int4-weight linear-projection library (gfx950).
+ *
+ * The paper runs the linear projections of a 175B-parameter decoder on
+ * 4-bit pre-quantized weights ("weight quantization", Sec. 2.2;
+ * "mixed-precision quantization", Sec. 3.1; "4-bit pre-quantized",
+ * Sec. 4.1) and attributes the GPU share of its runtime to that computation
+ * (Sec. 4.3).  The paper does not define the 4-bit scheme.  This library
+ * fixes it as follows, and every entry point below computes with it:
+ *
+ *   W        [N][K] fp32 weights, out = x * W^T (no bias).
+ *   group    g = 128 consecutive K elements of one weight row.
+ *   scale    s[n][j] = fp16_RNE(fp32(max_k |W[n][k]| / 7)), k in group j;
+ *            fp16 subnormals kept; overflow to inf is an error.
+ *   code     q[n][k] = clamp(rint_even(fp32(W[n][k] / s)), -8, 7), and 0 for
+ *            the whole group when s == 0.
+ *   qweight  uint8 [N][K/2]: byte i holds q[n][2i] in bits 0-3 and
+ *            q[n][2i+1] in bits 4-7, both 4-bit two's complement.
+ *   scales   uint16 [N][K/g]: binary16 bit patterns.
+ *   x, out   bf16 row-major bit patterns (uint16); accumulation is fp32 and
+ *            stored bf16 results are rounded to nearest even.
+ *
+ * Conventions for every entry point:
+ *   - All array pointers are DEVICE pointers (HIP device memory on the
+ *     current device) unless the comment says "host".  The caller owns every
+ *     buffer; the library never frees a caller buffer.
+ *   - Calls enqueue work on `stream` (NULL = the default stream) and return
+ *     without synchronising.  On a non-zero return nothing was enqueued.
+ *   - Shapes: M, N >= 1; K >= 128 and K % 128 == 0; group must be 128
+ *     (other group sizes return QL_ERR_UNSUPPORTED).  Ragged M and N are
+ *     handled by masking; no padding is required of the caller.
+ *   - Alignment: x and qweight must be 16-byte aligned and the row stride
+ *     of x (ldx) must keep every row 16-byte aligned; out needs only the
+ *     alignment of its element type (2 bytes bf16, 4 bytes fp32); scales 2
+ *     bytes (QL_ERR_ALIGN otherwise).
+ */
+#ifndef QLINEAR_H
+#define QLINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A hipStream_t; declared opaquely so this header needs no HIP headers. */
+typedef struct ihipStream_t* ql_stream_t;
+
+enum ql_status {
+    QL_OK = 0,
+    QL_ERR_ARG = 1,          /* null pointer, non-positive size, K % 128 != 0  */
+    QL_ERR_UNSUPPORTED = 2,  /* group != 128, or an unknown epilogue           */
+    QL_ERR_ALIGN = 3,        /* a pointer or row stride breaks 16 B alignment  */
+    QL_ERR_HIP = 4,          /* a HIP runtime call or a launch failed          */
+    QL_ERR_RANGE = 5,        /* pack: non-finite weight or fp16 scale overflow */
+    QL_ERR_WORKSPACE = 6     /* workspace pointer null or smaller than needed  */
+};
+
+enum ql_epilogue {
+    QL_EPI_NONE = 0,         /* out (bf16)  = acc                              */
+    QL_EPI_GELU = 1,         /* out (bf16)  = gelu_erf(acc)                    */
+    QL_EPI_RESID_F32 = 2     /* out (fp32) += acc   (residual stream update)   */
+};
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* qlinear_status_string(int status);
+
+/*
+ * qlinear_pack -- quantize fp32 weights into the packed int4 format above
+ * (the "pre-quantized" weights of Sec. 4.1).
+ *   w        [N][K] fp32, read only.
+ *   qweight  [N][K/2] uint8, written.
+ *   scales   [N][K/128] uint16 (binary16 bits), written.
+ *   status   nullable device int32.  When given, the kernel writes
+ *            QL_ERR_RANGE into it if any weight is non-finite or any scale
+ *            overflows fp16 (the caller zeroes it first and reads it after
+ *            synchronising).  The offending group's outputs are zero.
+ * Bit-exact: the division is IEEE fp32 (correctly rounded) on the device.
+ */
+int qlinear_pack(const float* w, uint8_t* qweight, uint16_t* scales,
+                 int64_t N, int64_t K, int32_t group, int32_t* status,
+                 ql_stream_t stream);
+
+/*
+ * qlinear_dequant -- W_dq[n][k] = fp32(q[n][k]) * fp32(s[n][k/128]), exact.
+ * Test and inspection export; the forward path never materialises W_dq.
+ *   w  [N][K] fp32, written.
+ */
+int qlinear_dequant(const uint8_t* qweight, const uint16_t* scales, float* w,
+                    int64_t N, int64_t K, int32_t group, ql_stream_t stream);
+
+/*
+ * qlinear_forward -- out[M][N] = bf16(x[M][K] * W_dq^T), the quantized
+ * linear projection of Sec. 3.3's "batch molecular encoding" forward pass.
+ * M <= 16 runs the bandwidth-bound small-batch kernel, larger M the
+ * MFMA tile kernel.  Uses a library-owned device workspace (grown on
+ * demand, one per device and stream, kept until qlinear_release); a call
+ * that must grow it synchronises `stream` and may allocate.  Callers that
+ * cannot allocate use qlinear_forward_ex with their own workspace.
+ *   x    [M][K] bf16 bits, contiguous.
+ *   out  [M][N] bf16 bits, contiguous, written.
+ */
+int qlinear_forward(const uint16_t* x, const uint8_t* qweight,
+                    const uint16_t* scales, uint16_t* out,
+                    int64_t M, int64_t N, int64_t K, int32_t group,
+                    ql_stream_t stream);
+
+/* Bytes of workspace qlinear_forward_ex needs for an M x K input. */
+size_t qlinear_workspace_bytes(int64_t M, int64_t K, int32_t group);
+
+/*
+ * qlinear_forward_ex -- qlinear_forward with strides, a fused epilogue and a
+ * caller-owned workspace; never allocates.
+ *   x          bf16 bits, row m at x + m*ldx (ldx >= K elements).
+ *   out        QL_EPI_NONE / QL_EPI_GELU: bf16 bits, row m at out + m*ldo
+ *              (uint16 elements).  QL_EPI_RESID_F32: fp32, row m at
+ *              (float*)out + m*ldo, read and updated in place.
+ *   workspace  device buffer of at least qlinear_workspace_bytes(M, K, g)
+ *              bytes, 256-byte aligned, used only while the enqueued work
+ *              runs; calls that overlap on one workspace race.
+ */
+int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
+                       const uint16_t* scales, void* out, int64_t ldo,
+                       int64_t M, int64_t N, int64_t K, int32_t group,
+                       int32_t epilogue, void* workspace, size_t ws_bytes,
+                       ql_stream_t stream);
+
+/* One packed weight matrix (device pointers). */
+typedef struct {
+    const uint8_t* qweight;
+    const uint16_t* scales;
+} ql_qmat;
+
+/*
+ * One block of the 175B-shaped linear stack (host struct of device
+ * pointers): qkv [3d][d], out [d][d], up [d_ff][d], down [d][d_ff].
+ * The QKV output columns are ordered [Q | K | V].
+ */
+typedef struct {
+    ql_qmat qkv, out, up, down;
+} ql_layer;
+
+/* Bytes of workspace qlayer_stack_forward needs. */
+size_t qlayer_stack_workspace_bytes(int64_t M, int64_t d, int64_t d_ff,
+                                    int32_t group);
+
+/*
+ * qlayer_stack_forward -- n_layers blocks of the linear stack on the fp32
+ * residual stream h [M][d] (updated in place).  Per block:
+ *     a   = bf16(RMSNorm(h))                 (unit gain, eps)
+ *     qkv = bf16(a * W_qkv^T)
+ *     v   = qkv[:, 2d:3d]                    (sliding-window attention of
+ *                                             width 1 is the identity on V;
+ *                                             the model of Sec. 1 / 2.1 uses
+ *                                             sliding-window attention)
+ *     h  += v * W_o^T                        (fp32)
+ *     a2  = bf16(RMSNorm(h))
+ *     u   = bf16(gelu_erf(a2 * W_up^T))
+ *     h  += u * W_down^T                     (fp32)
+ * All weights stay resident in device memory; nothing is paged from the
+ * host (the paper's Sec. 4.3 runtime split is dominated by such paging).
+ *   layers     HOST array of n_layers ql_layer structs.
+ *   workspace  >= qlayer_stack_workspace_bytes(M, d, d_ff, g) bytes,
+ *              256-byte aligned.  Layout (byte offsets, each 256-aligned):
+ *              [0]        a / a2 staging  bf16 [M][d]   (internal layout)
+ *              [qkv_off]  qkv             bf16 [M][3d]  (row-major)
+ *              [u_off]    u               bf16 [M][d_ff] (row-major)
+ *              then the correction terms; see qlayer_stack_workspace_offsets.
+ *   d, d_ff    multiples of 128.
+ */
+int qlayer_stack_forward(const ql_layer* layers, int32_t n_layers, float* h,
+                         int64_t M, int64_t d, int64_t d_ff, int32_t group,
+                         float eps, void* workspace, size_t ws_bytes,
+                         ql_stream_t stream);
+
+/*
+ * qlayer_stack_forward_timed -- qlayer_stack_forward with a timing hook for
+ * profilers and benchmarks.
+ *   events  nullable HOST array of 8 * n_layers hipEvent_t handles (as
+ *           void*; entries may be NULL).  events[8l + 2j] is recorded on
+ *           `stream` right before, and events[8l + 2j + 1] right after, the
+ *           launch of projection j of block l (j: 0 qkv, 1 out, 2 up,
+ *           3 down).  The caller creates and destroys the events.
+ */
+int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* h,
+                               int64_t M, int64_t d, int64_t d_ff, int32_t group,
+                               float eps, void* workspace, size_t ws_bytes,
+                               void* const* events, ql_stream_t stream);
+
+/* Host: byte offsets of the qkv and u buffers inside the stack workspace. */
+void qlayer_stack_workspace_offsets(int64_t M, int64_t d, int64_t d_ff,
+                                    int32_t group, size_t* qkv_off,
+                                    size_t* u_off);
+
+/*
+ * qlinear_rmsnorm -- a[m][k] = bf16(h[m][k] / sqrt(mean_k h[m][k]^2 + eps)),
+ * the normalisation between blocks of the stack.  Test export.
+ *   h  [M][d] fp32;  a  [M][d] bf16 bits, row-major, written.
+ */
+int qlinear_rmsnorm(const float* h, uint16_t* a, int64_t M, int64_t d,
+                    float eps, ql_stream_t stream);
+
+/* Frees the library-owned workspaces of qlinear_forward (synchronises the
+ * device first).  Safe to call at any time; later calls re-create them. */
+void qlinear_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLINEAR_H */

@@ -1,0 +1,247 @@
+"""Python binding of libqlinear (int4-weight linear projections on gfx950).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libqlinear.so`` behind the C ABI declared in ``include/qlinear.h``; torch
+supplies device memory and streams.  There is no CPU fallback: importing
+this package without the built library raises.
+
+bf16 tensors may be passed as ``torch.bfloat16`` or as their 16-bit patterns
+(``torch.int16`` / ``torch.uint16``); fp16 scales likewise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "LIB_PATH", "QLError", "lib", "GROUP", "EPI_NONE", "EPI_GELU", "EPI_RESID_F32",
+    "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
+    "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
+    "stack_forward_timed", "make_layers", "release",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
+GROUP = 128
+EPI_NONE, EPI_GELU, EPI_RESID_F32 = 0, 1, 2
+
+
+class QLError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: status {code} ({_status_string(code)})")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python paper_2608_30877_amd/build.py` "
+            "(there is no CPU fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    sig = {
+        "qlinear_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "qlinear_pack": (ctypes.c_int, [vp, vp, vp, i64, i64, i32, vp, vp]),
+        "qlinear_dequant": (ctypes.c_int, [vp, vp, vp, i64, i64, i32, vp]),
+        "qlinear_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, i64, i64, i32, vp]),
+        "qlinear_workspace_bytes": (sz, [i64, i64, i32]),
+        "qlinear_forward_ex": (ctypes.c_int, [vp, i64, vp, vp, vp, i64, i64, i64, i64, i32,
+                                              i32, vp, sz, vp]),
+        "qlayer_stack_workspace_bytes": (sz, [i64, i64, i64, i32]),
+        "qlayer_stack_workspace_offsets": (None, [i64, i64, i64, i32,
+                                                  ctypes.POINTER(sz), ctypes.POINTER(sz)]),
+        "qlayer_stack_forward": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
+                                                ctypes.c_float, vp, sz, vp]),
+        "qlayer_stack_forward_timed": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
+                                                      ctypes.c_float, vp, sz, vp, vp]),
+        "qlinear_rmsnorm": (ctypes.c_int, [vp, vp, i64, i64, ctypes.c_float, vp]),
+        "qlinear_release": (None, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def _status_string(code: int) -> str:
+    return lib.qlinear_status_string(int(code)).decode()
+
+
+def _check(code: int, where: str):
+    if code != 0:
+        raise QLError(code, where)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a CUDA (HIP) device")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D")
+
+
+_BITS16 = (torch.bfloat16, torch.int16, torch.uint16, torch.float16)
+
+
+class _QLayer(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "qkv_q", "qkv_s", "out_q", "out_s", "up_q", "up_s", "down_q", "down_s")]
+
+
+# ---------------------------------------------------------------------------
+
+def pack(w: torch.Tensor, group: int = GROUP, stream=None, check: bool = True):
+    """fp32 W [N, K] -> (qweight uint8 [N, K/2], scales int16 bits [N, K/g]).
+    With check=True, synchronises and raises QLError on QL_ERR_RANGE."""
+    _need(w, "w", (torch.float32,), 2)
+    w = w.contiguous()
+    N, K = w.shape
+    qw = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
+    sc = torch.empty((N, K // group), dtype=torch.int16, device=w.device)
+    status = torch.zeros(1, dtype=torch.int32, device=w.device)
+    _check(lib.qlinear_pack(_ptr(w), _ptr(qw), _ptr(sc), N, K, group, _ptr(status),
+                            _stream(stream)), "qlinear_pack")
+    if check:
+        code = int(status.item())
+        _check(code, "qlinear_pack (device status)")
+    return qw, sc
+
+
+def dequant(qweight: torch.Tensor, scales: torch.Tensor, group: int = GROUP, stream=None):
+    _need(qweight, "qweight", (torch.uint8,), 2)
+    _need(scales, "scales", _BITS16, 2)
+    N, H = qweight.shape
+    w = torch.empty((N, 2 * H), dtype=torch.float32, device=qweight.device)
+    _check(lib.qlinear_dequant(_ptr(qweight.contiguous()), _ptr(scales.contiguous()), _ptr(w),
+                               N, 2 * H, group, _stream(stream)), "qlinear_dequant")
+    return w
+
+
+def forward(x: torch.Tensor, qweight: torch.Tensor, scales: torch.Tensor,
+            out: torch.Tensor | None = None, group: int = GROUP, stream=None):
+    """out [M, N] bf16 = x [M, K] (bf16) @ dequant(qweight, scales)^T."""
+    _need(x, "x", _BITS16, 2)
+    _need(qweight, "qweight", (torch.uint8,), 2)
+    _need(scales, "scales", _BITS16, 2)
+    M, K = x.shape
+    N = qweight.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    _need(out, "out", _BITS16, 2)
+    _check(lib.qlinear_forward(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(out),
+                               M, N, K, group, _stream(stream)), "qlinear_forward")
+    return out
+
+
+def workspace_bytes(M: int, K: int, group: int = GROUP) -> int:
+    return int(lib.qlinear_workspace_bytes(M, K, group))
+
+
+def forward_ex(x, qweight, scales, out, epilogue: int = EPI_NONE, workspace=None,
+               M=None, N=None, K=None, ldx=None, ldo=None, group: int = GROUP, stream=None,
+               x_ptr=None):
+    """Strided / fused-epilogue forward with a caller workspace (uint8 tensor).
+    x may be a strided 2-D view (row stride ldx); out is bf16 for NONE/GELU
+    and fp32 (updated in place) for RESID_F32."""
+    M = x.shape[0] if M is None else M
+    K = x.shape[1] if K is None else K
+    N = qweight.shape[0] if N is None else N
+    ldx = x.stride(0) if ldx is None else ldx
+    ldo = out.stride(0) if ldo is None else ldo
+    xp = ctypes.c_void_p(x.data_ptr()) if x_ptr is None else ctypes.c_void_p(x_ptr)
+    ws_ptr = None if workspace is None else ctypes.c_void_p(workspace.data_ptr())
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.qlinear_forward_ex(xp, ldx, _ptr(qweight), _ptr(scales), _ptr(out), ldo,
+                                  M, N, K, group, epilogue, ws_ptr, ws_n, _stream(stream)),
+           "qlinear_forward_ex")
+    return out
+
+
+def rmsnorm(h: torch.Tensor, eps: float = 1e-5, stream=None):
+    _need(h, "h", (torch.float32,), 2)
+    M, d = h.shape
+    a = torch.empty((M, d), dtype=torch.bfloat16, device=h.device)
+    _check(lib.qlinear_rmsnorm(_ptr(h.contiguous()), _ptr(a), M, d, eps, _stream(stream)),
+           "qlinear_rmsnorm")
+    return a
+
+
+def stack_workspace_bytes(M: int, d: int, d_ff: int, group: int = GROUP) -> int:
+    return int(lib.qlayer_stack_workspace_bytes(M, d, d_ff, group))
+
+
+def stack_workspace_offsets(M: int, d: int, d_ff: int, group: int = GROUP):
+    q, u = ctypes.c_size_t(), ctypes.c_size_t()
+    lib.qlayer_stack_workspace_offsets(M, d, d_ff, group, ctypes.byref(q), ctypes.byref(u))
+    return int(q.value), int(u.value)
+
+
+def make_layers(layers):
+    """layers: list of dicts {"qkv": (qw, sc), "out": ..., "up": ..., "down": ...}
+    of device tensors -> ctypes array for stack_forward (keep the tensors alive)."""
+    arr = (_QLayer * len(layers))()
+    for i, L in enumerate(layers):
+        for name in ("qkv", "out", "up", "down"):
+            q, s = L[name]
+            setattr(arr[i], name + "_q", q.data_ptr())
+            setattr(arr[i], name + "_s", s.data_ptr())
+    return arr
+
+
+def stack_forward(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tensor,
+                  n_layers: int | None = None, eps: float = 1e-5, group: int = GROUP,
+                  stream=None):
+    """Run the linear stack in place on the fp32 residual h [M, d]."""
+    _need(h, "h", (torch.float32,), 2)
+    M, d = h.shape
+    n = len(layers_arr) if n_layers is None else n_layers
+    ws_n = workspace.numel() * workspace.element_size()
+    _check(lib.qlayer_stack_forward(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h), M, d,
+                                    d_ff, group, eps, _ptr(workspace), ws_n, _stream(stream)),
+           "qlayer_stack_forward")
+    return h
+
+
+def stack_forward_timed(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tensor,
+                        events, n_layers: int | None = None, eps: float = 1e-5,
+                        group: int = GROUP, stream=None):
+    """stack_forward with events: a list of 8 * n_layers torch.cuda.Event
+    (enable_timing=True) recorded around each projection launch."""
+    _need(h, "h", (torch.float32,), 2)
+    M, d = h.shape
+    n = len(layers_arr) if n_layers is None else n_layers
+    if len(events) != 8 * n:
+        raise ValueError("need 8 events per block")
+    st = torch.cuda.current_stream() if stream is None else stream
+    for e in events:                      # materialise the handles
+        if e.cuda_event == 0:
+            e.record(st)
+    ev_arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    ws_n = workspace.numel() * workspace.element_size()
+    _check(lib.qlayer_stack_forward_timed(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
+                                          M, d, d_ff, group, eps, _ptr(workspace), ws_n,
+                                          ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st)),
+           "qlayer_stack_forward_timed")
+    return h
+
+
+def release():
+    lib.qlinear_release()

@@ -1,0 +1,55 @@
+// Internal declarations shared by the HIP translation units of libqlinear.
+// Not part of the public ABI (see include/qlinear.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ql {
+
+constexpr int kGroup = 128;          // K elements per scale group
+constexpr int kGemmBM = 128;         // MFMA tile kernel: rows per workgroup
+constexpr int kGemmBN = 256;         //                   columns per workgroup
+constexpr int kSmallM = 16;          // M at or below this runs the small-batch kernel
+
+// Rows of the correction array are padded to this multiple.
+inline int64_t padded_rows(int64_t M) { return (M + kGemmBM - 1) / kGemmBM * kGemmBM; }
+
+// Bytes of the internal operand-staging area for an M x K activation:
+// the k-permuted bf16 copy [M][K] followed by the correction terms
+// fp32 [K/128][padded_rows(M)], each 256-byte aligned.
+inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+inline size_t xp_bytes(int64_t M, int64_t K) { return align256((size_t)M * K * 2); }
+inline size_t ns_bytes(int64_t M, int64_t K) {
+  return align256((size_t)(K / kGroup) * padded_rows(M) * 4);
+}
+
+// ---- launches (all asynchronous on `s`; return hipGetLastError()) ----
+
+hipError_t launch_pack(const float* w, uint8_t* qw, uint16_t* sc, int64_t N, int64_t K,
+                       int32_t* status, hipStream_t s);
+hipError_t launch_dequant(const uint8_t* qw, const uint16_t* sc, float* w, int64_t N,
+                          int64_t K, hipStream_t s);
+
+// x (bf16, row stride ldx) -> xp (k-permuted bf16 [M][K]) and
+// ns[g][m] = -136 * sum_{k in group g} x[m][k]   (fp32, row stride Mp)
+hipError_t launch_prep(const uint16_t* x, int64_t ldx, uint16_t* xp, float* ns, int64_t M,
+                       int64_t K, int64_t Mp, hipStream_t s);
+
+// RMSNorm of fp32 rows; `permuted` selects the MFMA operand layout (+ ns),
+// otherwise a plain row-major bf16 output (ns may be null).
+hipError_t launch_rmsnorm(const float* h, uint16_t* a, float* ns, int64_t M, int64_t d,
+                          int64_t Mp, float eps, bool permuted, hipStream_t s);
+
+// Large-M MFMA kernel on prepared operands.
+hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
+                       const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
+                       int64_t K, int epilogue, hipStream_t s);
+
+// Small-M kernel on raw bf16 activations (M <= kSmallM).
+hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
+                       void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
+                       hipStream_t s);
+
+}  // namespace ql

@@ -101,3 +101,10 @@ def weights_f32_cuda(seed: int, N: int, K: int, std: float = 0.02, out=None):
         out = torch.empty((N, K), dtype=torch.float32, device="cuda")
     out.normal_(0.0, std, generator=g)
     return out
+
+
+def random_scales_f16(seed: int, N: int, G: int, lo: float = 0.004, hi: float = 0.016) -> np.ndarray:
+    """[N, G] binary16 bits of scales uniform in [lo, hi] (the range that
+    N(0, 0.02) weights give), for packed weights drawn directly as bytes."""
+    v = _rng(seed + 10_000_000).uniform(lo, hi, size=(N, G)).astype(np.float32)
+    return v.astype(np.float16).view(np.uint16)

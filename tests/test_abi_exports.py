@@ -1,0 +1,100 @@
+"""The C-ABI library loads, exports every symbol that include/qlinear.h
+declares, and rejects bad arguments before touching the GPU (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlinear.h")
+LIB = os.path.join(ROOT, "paper_2608_30877_amd", "libqlinear.so")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\**\s+\**([a-z][a-z0-9_]*)\s*\(",
+                       src, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail(f"{LIB} not built (run python paper_2608_30877_amd/build.py)")
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for need in ["qlinear_pack", "qlinear_forward", "qlayer_stack_forward", "qlinear_dequant",
+                 "qlinear_forward_ex", "qlinear_workspace_bytes", "qlinear_status_string",
+                 "qlayer_stack_workspace_bytes", "qlinear_rmsnorm", "qlinear_release",
+                 "qlayer_stack_workspace_offsets"]:
+        assert need in names, need
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"libqlinear.so does not export {name}"
+
+
+def test_status_strings(lib):
+    f = lib.qlinear_status_string
+    f.restype = ctypes.c_char_p
+    f.argtypes = [ctypes.c_int]
+    assert f(0) == b"ok"
+    for code in range(1, 7):
+        assert f(code) and f(code) != b"unknown status"
+    assert f(99) == b"unknown status"
+
+
+def _fwd(lib):
+    f = lib.qlinear_forward
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    f.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp]
+    f.restype = ctypes.c_int
+    return f
+
+
+def test_argument_errors_without_launch(lib):
+    f = _fwd(lib)
+    p = ctypes.c_void_p(4096)          # never dereferenced: validation fails first
+    assert f(None, p, p, p, 4, 4, 128, 128, None) == 1           # null pointer
+    assert f(p, p, p, p, 0, 4, 128, 128, None) == 1              # M <= 0
+    assert f(p, p, p, p, 4, 4, 100, 128, None) == 1              # K % 128
+    assert f(p, p, p, p, 4, 4, 128, 64, None) == 2               # group != 128
+    odd = ctypes.c_void_p(4096 + 8)
+    assert f(odd, p, p, p, 4, 4, 128, 128, None) == 3            # misaligned x
+
+
+def test_forward_ex_errors_without_launch(lib):
+    f = lib.qlinear_forward_ex
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, i64, i32, i32, vp, sz, vp]
+    f.restype = ctypes.c_int
+    p = ctypes.c_void_p(4096)
+    # unknown epilogue
+    assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 7, p, 1 << 20, None) == 2
+    # ldx smaller than K
+    assert f(p, 64, p, p, p, 64, 64, 64, 128, 128, 0, p, 1 << 20, None) == 1
+    # M > 16 needs a workspace
+    assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 0, None, 0, None) == 6
+    ws = lib.qlinear_workspace_bytes
+    ws.argtypes = [i64, i64, i32]
+    ws.restype = sz
+    assert ws(16, 4096, 128) == 0                     # small-M path uses none
+    assert ws(2048, 12288, 128) >= 2048 * 12288 * 2   # permuted activation copy
+    assert ws(4, 100, 128) == 0                        # invalid shape -> 0
+
+
+def test_stack_errors_without_launch(lib):
+    f = lib.qlayer_stack_forward
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i32, vp, i64, i64, i64, i32, ctypes.c_float, vp, sz, vp]
+    f.restype = ctypes.c_int
+    p = ctypes.c_void_p(4096)
+    assert f(None, 1, p, 8, 256, 512, 128, 1e-5, p, 1 << 30, None) == 1
+    assert f(p, 1, p, 8, 200, 512, 128, 1e-5, p, 1 << 30, None) == 1      # d % 128
+    assert f(p, 1, p, 8, 256, 512, 128, 1e-5, p, 16, None) == 6           # workspace

@@ -1,0 +1,313 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bars: bit-exact for packing and dequantization; bit-exact for the exact-
+arithmetic inputs (ternary x, uniform codes, power-of-two scales: every
+partial sum is an exact fp32 value in any order); relative Frobenius error
+<= 5e-3 for bf16 outputs on workload-like inputs (the tolerance the path is
+specified with).  Full-size problems are checked on sampled output columns
+that the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from tests.gpu_util import bf16_as_f64, dev, dev_u16, host_u16, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 5e-3
+# Non-exact inputs: the kernels feed 136 + q to the MFMA and remove 136 * sum(x)
+# per group, so a group's dot product carries an absolute error of a few fp32
+# ulps of 136 * |sum x| (~1e-4 for N(0,1) x), which flips the bf16 rounding of
+# a small fraction of outputs by one ulp: ~1e-5 .. 1e-4 relative Frobenius.
+OFFSET_TOL = 2e-4
+
+
+@pytest.fixture(scope="module")
+def ql():
+    import paper_2608_30877_amd as ql
+
+    return ql
+
+
+def _pack_gpu(ql, w):
+    qw, sc = ql.pack(dev(w))
+    torch.cuda.synchronize()
+    return qw.cpu().numpy(), host_u16(sc)
+
+
+# ------------------------------------------------------------------ pack / dequant
+
+@pytest.mark.parametrize("N,K", [(512, 512), (3, 128), (77, 384), (256, 12288)])
+def test_pack_bit_exact(ql, N, K):
+    say(f"pack N={N} K={K}")
+    w = synth.weights_f32(100 + N, N, K)
+    qw_ref, sc_ref = O.quantize_pack(w)
+    qw, sc = _pack_gpu(ql, w)
+    np.testing.assert_array_equal(sc, sc_ref)
+    np.testing.assert_array_equal(qw, qw_ref)
+
+
+def test_pack_edge_groups_bit_exact(ql):
+    """Ties, zero groups, subnormal and tiny scales, the largest scale, and
+    a coarse subnormal scale that clamps to -8."""
+    w = np.zeros((8, 256), dtype=np.float32)
+    w[0, :7] = [7.0, 2.5, -2.5, 3.5, 0.5, 1.5, -1.5]
+    w[1, 5] = np.float32(7 * 2.0 ** -25)
+    w[2, 5] = np.float32(7 * 2.0 ** -25) * np.float32(1.0001)
+    w[2, 6] = -w[2, 5]
+    a = np.float32(7 * 1.4 * 2.0 ** -24)
+    w[3, 0], w[3, 1] = a, -a
+    w[4, 3] = np.float32(7 * 65504.0)
+    w[5] = synth.weights_f32(5, 1, 256)[0] * np.float32(3e-6)
+    w[6] = synth.weights_f32(6, 1, 256)[0] * np.float32(1e3)
+    w[7, 128:] = -np.float32(0.75)
+    qw_ref, sc_ref = O.quantize_pack(w)
+    qw, sc = _pack_gpu(ql, w)
+    np.testing.assert_array_equal(sc, sc_ref)
+    np.testing.assert_array_equal(qw, qw_ref)
+
+
+@pytest.mark.parametrize("bad", [np.nan, np.inf, 7 * 65520.0])
+def test_pack_range_error(ql, bad):
+    w = synth.weights_f32(7, 4, 256)
+    w[2, 100] = np.float32(bad)
+    with pytest.raises(ql.QLError) as e:
+        ql.pack(dev(w))
+    assert e.value.code == 5
+
+
+def test_pack_full_qkv_shape_bit_exact(ql):
+    """The QKV projection at 175B width: N = 36864, K = 12288."""
+    N, K = 36864, 12288
+    say(f"pack full N={N} K={K}")
+    w = synth.weights_f32(synth.matrix_seed(synth.SEED_QKV, 0, 0), N, K)
+    qw, sc = _pack_gpu(ql, w)
+    for r0 in range(0, N, 6144):      # oracle in row blocks to bound host memory
+        qr, sr = O.quantize_pack(w[r0:r0 + 6144])
+        np.testing.assert_array_equal(sc[r0:r0 + 6144], sr)
+        np.testing.assert_array_equal(qw[r0:r0 + 6144], qr)
+
+
+@pytest.mark.parametrize("N,K", [(512, 512), (96, 1280)])
+def test_dequant_bit_exact(ql, N, K):
+    qw = synth.random_packed_bytes(N + K, N, K)
+    sc = O.quantize_pack(synth.weights_f32(N, N, K))[1]
+    w = ql.dequant(dev(qw), dev_u16(sc)).cpu().numpy()
+    np.testing.assert_array_equal(w, O.dequant(qw, sc))
+
+
+# ------------------------------------------------------------------ forward
+
+SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel, ragged tails
+    (1, 64, 128), (5, 250, 384), (8, 512, 512), (16, 512, 512), (16, 1000, 1280),
+    (17, 256, 256), (64, 384, 512), (128, 256, 512), (200, 500, 640), (300, 1024, 1152),
+]
+
+
+def _forward_np(ql, x, qw, sc):
+    y = ql.forward(dev_u16(x), dev(qw), dev_u16(sc))
+    torch.cuda.synchronize()
+    return host_u16(y)
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_forward_exact_arithmetic_bit_exact(ql, M, N, K):
+    """x in {-1,0,1}, uniform codes, s = 2^-3: out == bf16(int matmul / 8)."""
+    say(f"exact M={M} N={N} K={K}")
+    x = synth.ternary_bf16(M * 7 + N, M, K)
+    qw = synth.random_packed_bytes(M + N * 3, N, K)
+    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
+    np.testing.assert_array_equal(_forward_np(ql, x, qw, sc), ref)
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_forward_workload_inputs(ql, M, N, K):
+    say(f"forward M={M} N={N} K={K}")
+    x = synth.activations_bf16(M + 11 * N, M, K, outlier_frac=0.01)
+    qw, sc = O.quantize_pack(synth.weights_f32(N + 13 * M, N, K))
+    y = bf16_as_f64(_forward_np(ql, x, qw, sc))
+    assert O.rel_fro(y, O.qlinear_ref(x, qw, sc)) <= TOL
+
+
+def test_forward_toy_config(ql):
+    """M = 16 tokens, K = N = 512, N(0,0.02) weights, N(0,1) activations."""
+    x = synth.activations_bf16(synth.SEED_TOY, 16, 512)
+    qw, sc = O.quantize_pack(synth.weights_f32(synth.SEED_TOY, 512, 512))
+    y = bf16_as_f64(_forward_np(ql, x, qw, sc))
+    assert O.rel_fro(y, O.qlinear_ref(x, qw, sc)) <= TOL
+
+
+@pytest.mark.parametrize("M", [8, 200])
+def test_zero_scales_zero_output(ql, M):
+    x = synth.activations_bf16(M, M, 512)
+    qw = synth.random_packed_bytes(M, 384, 512)
+    sc = synth.const_f16_bits(384, 4, 0)
+    assert not _forward_np(ql, x, qw, sc).any()
+
+
+def _grid_bf16(seed, M, K):
+    """x = k/16 with integer k in [-128, 128]: exact in bf16, and every group
+    sum of 136*x + q*x is an exact fp32 value."""
+    k = np.random.default_rng(seed).integers(-128, 129, (M, K))
+    return O.f64_to_bf16_bits(k / 16.0)
+
+
+@pytest.mark.parametrize("M", [3, 16, 130])
+def test_identity_and_permutation(ql, M):
+    """q = 1 on a permuted diagonal, s = 1: out == x[:, perm] bit for bit on
+    grid-valued x, and within tolerance on N(0,1) x."""
+    K = 512
+    perm = np.random.default_rng(M).permutation(K)
+    q = np.zeros((K, K), dtype=np.int64)
+    q[np.arange(K), perm] = 1
+    nib = (q & 0xF).astype(np.uint8)
+    qw = (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+    sc = synth.const_f16_bits(K, K // 128, 0x3C00)
+    xg = _grid_bf16(M, M, K)
+    np.testing.assert_array_equal(_forward_np(ql, xg, qw, sc), xg[:, perm])
+    x = synth.activations_bf16(M + 1, M, K)
+    y = bf16_as_f64(_forward_np(ql, x, qw, sc))
+    assert O.rel_fro(y, bf16_as_f64(x[:, perm])) <= OFFSET_TOL
+
+
+@pytest.mark.parametrize("M", [7, 256])
+def test_sign_symmetry(ql, M):
+    """forward(x, -q) == -forward(x, q) bit for bit on exact-arithmetic inputs
+    (codes in [-7, 7] built through the packer's round trip), and to rounding
+    on workload inputs."""
+    K, N = 640, 320
+    rng = np.random.default_rng(M)
+    q = rng.integers(-7, 8, (N, K))
+    q[:, ::128] = 7
+    w = (q * 0.125).astype(np.float32)
+    qw, sc = O.quantize_pack(w)
+    qn, sn = O.quantize_pack(-w)
+    x = synth.ternary_bf16(M + 3, M, K)
+    a = _forward_np(ql, x, qw, sc)
+    b = _forward_np(ql, x, qn, sn)
+    np.testing.assert_array_equal(bf16_as_f64(b), -bf16_as_f64(a))
+    xw = synth.activations_bf16(M + 5, M, K)
+    qw, sc = O.quantize_pack(synth.weights_f32(M + 4, N, K))
+    qn, sn = O.quantize_pack(-synth.weights_f32(M + 4, N, K))
+    a = bf16_as_f64(_forward_np(ql, xw, qw, sc))
+    b = bf16_as_f64(_forward_np(ql, xw, qn, sn))
+    assert O.rel_fro(-b, a) <= OFFSET_TOL
+
+
+@pytest.mark.parametrize("epi", [1, 2])
+@pytest.mark.parametrize("M", [12, 160])
+def test_forward_ex_epilogues_and_strides(ql, epi, M):
+    """GELU (bf16 out) and fp32 residual-add epilogues, strided x and out."""
+    K, N = 512, 384
+    xfull = synth.activations_bf16(M + epi, M, K + 256)
+    x = xfull[:, 64:64 + K]
+    qw, sc = O.quantize_pack(synth.weights_f32(M * epi, N, K))
+    ref = O.qlinear_ref(np.ascontiguousarray(x), qw, sc)
+    xd = dev_u16(xfull)
+    xv = xd[:, 64:64 + K]
+    ws = torch.empty(max(ql.workspace_bytes(M, K), 1), dtype=torch.uint8, device="cuda")
+    if epi == 1:
+        out = torch.zeros((M, N + 64), dtype=torch.bfloat16, device="cuda")
+        ql.forward_ex(xv, dev(qw), dev_u16(sc), out[:, :N], ql.EPI_GELU, ws, ldo=N + 64)
+        y = bf16_as_f64(host_u16(out)[:, :N])
+        assert O.rel_fro(y, O.gelu(ref)) <= TOL
+        assert not host_u16(out)[:, N:].any()
+    else:
+        h0 = synth.residual_f32(M, M, N + 64)
+        hd = dev(h0)
+        ql.forward_ex(xv, dev(qw), dev_u16(sc), hd[:, :N], ql.EPI_RESID_F32, ws, ldo=N + 64)
+        h = hd.cpu().numpy()
+        np.testing.assert_array_equal(h[:, N:], h0[:, N:])
+        assert O.rel_fro(h[:, :N] - h0[:, :N], ref) <= 1e-4
+
+
+# ------------------------------------------------------------------ full-size configs
+
+def _sampled(N, n, seed):
+    return np.sort(np.random.default_rng(seed).choice(N, n, replace=False))
+
+
+def _full_case(ql, M, N, K, seed, outliers, epi=0, nsamp=96, x=None):
+    """Weights drawn on the device by the seeded generator; the sampled rows
+    are copied to the host, packed by the oracle (and compared with the
+    device packing), and the sampled output columns are recomputed by the
+    oracle from the same x."""
+    say(f"full M={M} N={N} K={K} epi={epi}")
+    if x is None:
+        x = synth.activations_bf16(seed, M, K, outlier_frac=0.01 if outliers else 0.0)
+    wd = synth.weights_f32_cuda(synth.matrix_seed(seed, 0, 0), N, K)
+    qw, sc = ql.pack(wd)
+    cols = _sampled(N, nsamp, seed)
+    ci = torch.from_numpy(cols).cuda()
+    w_rows = wd[ci].cpu().numpy()
+    del wd
+    xd = dev_u16(x)
+    if epi == 0:
+        y = ql.forward(xd, qw, sc)
+    else:
+        ws = torch.empty(max(ql.workspace_bytes(M, K), 1), dtype=torch.uint8, device="cuda")
+        y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        ql.forward_ex(xd, qw, sc, y, epi, ws)
+    torch.cuda.synchronize()
+    qr, sr = O.quantize_pack(w_rows)
+    np.testing.assert_array_equal(qw[ci].cpu().numpy(), qr)
+    np.testing.assert_array_equal(host_u16(sc[ci]), sr)
+    ys = bf16_as_f64(host_u16(y[:, ci]))
+    ref = O.qlinear_ref(x, qr, sr)
+    if epi == 1:
+        ref = O.gelu(ref)
+    return O.rel_fro(ys, ref)
+
+
+def test_full_qkv_prefill(ql):
+    """QKV at 175B width, prefill: M = 2048, K = 12288, N = 36864, outliers."""
+    assert _full_case(ql, 2048, 36864, 12288, synth.SEED_QKV, True) <= TOL
+
+
+def test_full_ffn_up_gelu(ql):
+    """FFN up-projection with the GELU epilogue: M = 2048, K = 12288, N = 49152."""
+    assert _full_case(ql, 2048, 49152, 12288, synth.SEED_FFN, False, epi=1) <= TOL
+
+
+def test_full_ffn_down(ql):
+    """FFN down-projection: M = 2048, K = 49152, N = 12288 (bf16 N(0,1) input
+    of the shape of the GELU output)."""
+    x = synth.activations_bf16(synth.SEED_FFN + 50, 2048, 49152)
+    assert _full_case(ql, 2048, 12288, 49152, synth.SEED_FFN + 1, False, nsamp=48, x=x) <= TOL
+
+
+def test_full_small_batch(ql):
+    """Bandwidth-bound regime: M = 8, K = 12288, N = 49152."""
+    assert _full_case(ql, 8, 49152, 12288, synth.SEED_GEMV, False, nsamp=512) <= TOL
+
+
+@pytest.mark.parametrize("M,N,K", [(2048, 12288, 49152), (8, 49152, 12288)])
+def test_full_exact_arithmetic_bit_exact(ql, M, N, K):
+    """Exact-arithmetic inputs at full size (K = 49152 is the longest
+    reduction: partial sums stay below 2^24 quanta of 2^-3)."""
+    say(f"full exact M={M} N={N} K={K}")
+    x = synth.ternary_bf16(9, M, K)
+    qw = synth.random_packed_bytes(9, N, K)
+    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    y = ql.forward(dev_u16(x), dev(qw), dev_u16(sc))
+    torch.cuda.synchronize()
+    cols = _sampled(N, 64, 9)
+    ci = torch.from_numpy(cols).cuda()
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw[cols], sc[cols]))
+    np.testing.assert_array_equal(host_u16(y[:, ci]), ref)
+
+
+# ------------------------------------------------------------------ RMSNorm
+
+@pytest.mark.parametrize("M,d", [(3, 256), (64, 12288)])
+def test_rmsnorm(ql, M, d):
+    h = synth.residual_f32(M + d, M, d) * np.float32(3.0)
+    a = host_u16(ql.rmsnorm(dev(h)))
+    ref = O.rmsnorm_bf16(h)
+    diff = np.abs(a.astype(np.int32) - ref.astype(np.int32))
+    assert diff.max() <= 1                       # at most one bf16 ulp
+    assert (diff > 0).mean() < 1e-3
