@@ -108,18 +108,23 @@ class _QLayer(ctypes.Structure):
 
 # ---------------------------------------------------------------------------
 
-def pack(w: torch.Tensor, group: int = GROUP, stream=None, check: bool = True):
+def pack(w: torch.Tensor, group: int = GROUP, stream=None, check: bool = True,
+         status: torch.Tensor | None = None):
     """fp32 W [N, K] -> (qweight uint8 [N, K/2], scales int16 bits [N, K/g]).
-    With check=True, synchronises and raises QLError on QL_ERR_RANGE."""
+    Without `status`, synchronises and raises QLError on QL_ERR_RANGE (when
+    check=True).  With a caller's zeroed int32 device `status`, nothing is
+    synchronised and the kernel writes QL_ERR_RANGE into it on a range error."""
     _need(w, "w", (torch.float32,), 2)
     w = w.contiguous()
     N, K = w.shape
     qw = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
     sc = torch.empty((N, K // group), dtype=torch.int16, device=w.device)
-    status = torch.zeros(1, dtype=torch.int32, device=w.device)
+    own = status is None
+    if own:
+        status = torch.zeros(1, dtype=torch.int32, device=w.device)
     _check(lib.qlinear_pack(_ptr(w), _ptr(qw), _ptr(sc), N, K, group, _ptr(status),
                             _stream(stream)), "qlinear_pack")
-    if check:
+    if own and check:
         code = int(status.item())
         _check(code, "qlinear_pack (device status)")
     return qw, sc
