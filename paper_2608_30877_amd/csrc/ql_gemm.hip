@@ -2,20 +2,24 @@
 //
 // out[m][n] = sum_g s[n][g] * sum_{k in g} x[m][k] * q[n][k]
 //
-// Each workgroup (4 waves) owns a 128 x 256 output tile; wave w owns the
-// 128 x 64 column slice [64w, 64w+64).  The K loop walks one 128-wide scale
-// group per step:
-//   * the activation tile (128 rows x 128 k, pre-permuted bf16) and the
-//     packed weight tile (256 columns x 64 bytes) are copied global -> LDS
-//     with direct-to-LDS loads, double-buffered, one group ahead;
-//   * each wave unpacks its 64 x 128 int4 codes once into bf16 values
+// Each workgroup (8 waves, two per SIMD) owns a 128 x 256 output tile; wave
+// w owns the 128 x 32 column slice [32w, 32w+32).  The K loop walks one
+// 128-wide scale group per step:
+//   * the activation tile (128 rows x 128 k, pre-permuted bf16), the packed
+//     weight tile (256 columns x 64 bytes), the group's 256 scales and 128
+//     correction terms are copied global -> LDS with direct-to-LDS loads,
+//     double-buffered, one group ahead (no register holds in-flight data, so
+//     no wait is needed before the end of the step);
+//   * each wave unpacks its 32 x 128 int4 codes once into bf16 values
 //     136 + q (exact; see unpack_offset_codes) and reuses them for all 8
 //     row fragments;
 //   * per 16 x 16 output fragment, a chain of four 16x16x32 MFMAs covers the
 //     group.  The chain starts from the correction -136 * sum_k x[m][k], so
-//     its result is exactly the integer-code dot product sum x*q (fp32), and
-//     one fp32 FMA applies the group's scale: acc += chain * s[n][g].
+//     its result is the integer-code dot product sum x*q (fp32), and one fp32
+//     FMA applies the group's scale: acc += chain * s[n][g].
 // Scales therefore stay exact fp32 (no bf16 rounding of q*s).
+#include <algorithm>
+
 #include "ql_device.h"
 #include "ql_internal.h"
 
@@ -23,10 +27,17 @@ namespace ql {
 
 namespace {
 
+constexpr int NW = 8;                  // waves per workgroup
+constexpr int WN = 32;                 // columns per wave
+constexpr int JF = WN / 16;            // 16-column fragments per wave
 constexpr int BM = kGemmBM;            // 128
-constexpr int BN = kGemmBN;            // 256
+constexpr int BN = NW * WN;            // 256
 constexpr int A_SLOTS = BM * 16;       // 16-byte slots per stage (32 KB)
 constexpr int B_SLOTS = BN * 4;        // 16 KB
+constexpr int A_PER_WAVE = A_SLOTS / 64 / NW;   // 4 direct-to-LDS loads per wave
+constexpr int B_PER_WAVE = B_SLOTS / 64 / NW;   // 2
+constexpr int S_WAVES = BN / 64;                // waves that copy the scales
+static_assert(BN == kGemmBN, "tile width");
 
 struct GemmParams {
   const uint16_t* xp;
@@ -39,53 +50,54 @@ struct GemmParams {
   int tiles_m, tiles_n;
 };
 
-// LDS slot swizzles (conflict-free 16-byte reads for 32- and 64-bank LDS).
-__device__ __forceinline__ int a_phys(int row, int chunk) { return chunk ^ (row & 15); }
-__device__ __forceinline__ int b_phys(int col, int h) { return h ^ (((col >> 1) ^ (col >> 2)) & 3); }
+// LDS slot swizzles.  gfx950 serves a 16-byte-per-lane LDS read in four
+// cycles; one cycle takes the 4-lane quads of a half-wave whose quad index
+// (lane bits 2-4) has a given parity, so a pattern is conflict-free when each
+// such set of 16 lanes covers all 16 slots of a 256-byte bank row.  Row r of
+// the activation tile stores logical 16-byte chunk c at slot c ^ a_msk(r);
+// column n of the weight tile stores its 16-byte piece h at slot h ^ b_swz(n).
+__device__ __forceinline__ int a_msk(int row) {
+  row &= 15;
+  return row ^ ((((row >> 2) ^ (row >> 3)) & 1) << 2);
+}
+__device__ __forceinline__ int a_phys(int row, int chunk) { return chunk ^ a_msk(row); }
+__device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2)) & 3; }
 
-__device__ __forceinline__ void issue_stage(const GemmParams& p, int64_t m0, int64_t n0, int g,
-                                            u32x4* sA, u32x4* sB, float* sN, int wave, int lane) {
-  // activations: 8 wave-instructions of 64 x 16 B
+struct Offsets {
+  uint32_t a[A_PER_WAVE];  // byte offsets into xp of this lane's A slots (group 0)
+  uint32_t b[B_PER_WAVE];  // byte offsets into qw of this lane's B slots (group 0)
+};
+
+__device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets& o, uint32_t os,
+                                            int64_t m0, int g, u32x4* sA, u32x4* sB, float* sN,
+                                            uint32_t* sS, int wave, int lane) {
+  const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
+  const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int base = (j * 4 + wave) * 64;
-    const int slot = base + lane;
-    const int row = slot >> 4;
-    const int chunk = (slot & 15) ^ (row & 15);
-    const int64_t gm = min<int64_t>(m0 + row, p.M - 1);
-    const uint16_t* src = p.xp + gm * p.K + (int64_t)g * kGroup + chunk * 8;
-    __builtin_amdgcn_global_load_lds(src, sA + base, 16, 0, 0);
-  }
-  // packed weights: 4 wave-instructions of 64 x 16 B
+  for (int j = 0; j < A_PER_WAVE; ++j)
+    __builtin_amdgcn_global_load_lds(xa + o.a[j], sA + (j * NW + wave) * 64, 16, 0, 0);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int base = (j * 4 + wave) * 64;
-    const int slot = base + lane;
-    const int col = slot >> 2;
-    const int h = (slot & 3) ^ (((col >> 1) ^ (col >> 2)) & 3);
-    const int64_t gn = min<int64_t>(n0 + col, p.N - 1);
-    const uint8_t* src = p.qw + gn * (p.K / 2) + (int64_t)g * (kGroup / 2) + h * 16;
-    __builtin_amdgcn_global_load_lds(src, sB + base, 16, 0, 0);
-  }
-  // correction terms of the 128 rows
+  for (int j = 0; j < B_PER_WAVE; ++j)
+    __builtin_amdgcn_global_load_lds(qb + o.b[j], sB + (j * NW + wave) * 64, 16, 0, 0);
   if (wave == 0) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const float* src = p.ns + (int64_t)g * p.Mp + m0 + j * 64 + lane;
-      __builtin_amdgcn_global_load_lds(src, sN + j * 64, 4, 0, 0);
-    }
+    const float* src = p.ns + (size_t)g * p.Mp + m0 + lane;
+    __builtin_amdgcn_global_load_lds(src, sN, 4, 0, 0);
+    __builtin_amdgcn_global_load_lds(src + 64, sN + 64, 4, 0, 0);
   }
+  // scales: a 2-byte direct-to-LDS copy lands zero-extended in one dword per
+  // lane; wave w < S_WAVES copies columns [64w, 64w+64) of the tile
+  if (wave < S_WAVES) __builtin_amdgcn_global_load_lds(p.sc + os + g, sS + wave * 64, 2, 0, 0);
 }
 
 template <int EPI>
 __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, const f32x4 (&acc)[8][4]) {
+                                           int lane, const f32x4 (&acc)[8][JF]) {
   const int h = lane >> 4, lr = lane & 15;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t col = n0 + wave * 64 + j * 16 + lr;
+    for (int j = 0; j < JF; ++j) {
+      const int64_t col = n0 + wave * WN + j * 16 + lr;
       if (col >= p.N) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -105,15 +117,29 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
   }
 }
 
-__device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, const float* sN,
-                                              const float (&scf)[4], int wave, int lane,
-                                              f32x4 (&acc)[8][4]) {
-  const int h = lane >> 4, lr = lane & 15;
-  bf16x8 bq[4][4];
+__device__ __forceinline__ void load_a(const u32x4* sA, const float* sN, int i, int h, int lr,
+                                       bf16x8 (&a)[4], f32x4& n4) {
+  const int row = i * 16 + lr;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int col = wave * 64 + j * 16 + lr;
-    const u32x4 raw = sB[col * 4 + b_phys(col, h)];
+  for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(sA[row * 16 + a_phys(row, h * 4 + s)]);
+  n4 = *reinterpret_cast<const f32x4*>(sN + i * 16 + h * 4);
+}
+
+__device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, const float* sN,
+                                              const uint32_t* sS, int wave, int lane,
+                                              f32x4 (&acc)[8][JF]) {
+  const int h = lane >> 4, lr = lane & 15;
+  float scf[JF];
+#pragma unroll
+  for (int j = 0; j < JF; ++j) scf[j] = f16_to_f32((uint16_t)sS[wave * WN + j * 16 + lr]);
+  bf16x8 a[4], an[4];
+  f32x4 n4, nn;
+  load_a(sA, sN, 0, h, lr, a, n4);
+  bf16x8 bq[JF][4];
+#pragma unroll
+  for (int j = 0; j < JF; ++j) {
+    const int col = wave * WN + j * 16 + lr;
+    const u32x4 raw = sB[col * 4 + (h ^ b_swz(col))];
     bq[j][0] = unpack_offset_codes(raw.x);
     bq[j][1] = unpack_offset_codes(raw.y);
     bq[j][2] = unpack_offset_codes(raw.z);
@@ -121,33 +147,41 @@ __device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, 
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int row = i * 16 + lr;
-    const f32x4 n4 = *reinterpret_cast<const f32x4*>(sN + i * 16 + h * 4);
-    bf16x8 a[4];
+    if (i + 1 < 8) load_a(sA, sN, i + 1, h, lr, an, nn);
+    f32x4 c[JF];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(sA[row * 16 + a_phys(row, h * 4 + s)]);
-    f32x4 c[4] = {n4, n4, n4, n4};
+    for (int j = 0; j < JF; ++j) c[j] = n4;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) c[j] = mfma16x16x32(a[s], bq[j][s], c[j]);
+      for (int j = 0; j < JF; ++j) c[j] = mfma16x16x32(a[s], bq[j][s], c[j]);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] += c[j] * scf[j];
+    for (int j = 0; j < JF; ++j) acc[i][j] += c[j] * scf[j];
+    if (i + 1 < 8) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) a[s] = an[s];
+      n4 = nn;
+    }
+    // keep the row fragments in program order: hoisting later fragments'
+    // LDS reads above this point would only raise register pressure
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 template <int EPI>
-__global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
+__global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   __shared__ u32x4 sA0[A_SLOTS];
   __shared__ u32x4 sA1[A_SLOTS];
   __shared__ u32x4 sB0[B_SLOTS];
   __shared__ u32x4 sB1[B_SLOTS];
   __shared__ float sN0[BM];
   __shared__ float sN1[BM];
+  __shared__ uint32_t sS0[BN];
+  __shared__ uint32_t sS1[BN];
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, lr = lane & 15;
 
   // workgroup -> tile: first spread consecutive tiles over the 8 XCDs'
   // dispatch order so that each XCD sees a contiguous tile range, then walk
@@ -165,85 +199,100 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmParams p) {
   const int64_t m0 = (int64_t)(first_m + in_grp % gm) * BM;
   const int64_t n0 = (int64_t)(in_grp / gm) * BN;
 
-  // scale pointers of this lane's four 16-column fragments
-  const uint16_t* srow[4];
+  // per-lane source offsets of the direct-to-LDS copies (rows and columns
+  // past the matrix edge are clamped: they load valid memory and their
+  // results are never stored)
+  Offsets o;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t col = min<int64_t>(n0 + wave * 64 + j * 16 + lr, p.N - 1);
-    srow[j] = p.sc + col * p.G;
+  for (int j = 0; j < A_PER_WAVE; ++j) {
+    const int slot = (j * NW + wave) * 64 + lane;
+    const int row = slot >> 4;
+    const int chunk = (slot & 15) ^ a_msk(row);
+    const int64_t r = min<int64_t>(m0 + row, p.M - 1);
+    o.a[j] = (uint32_t)((r * p.K + chunk * 8) * 2);
   }
+#pragma unroll
+  for (int j = 0; j < B_PER_WAVE; ++j) {
+    const int slot = (j * NW + wave) * 64 + lane;
+    const int col = slot >> 2;
+    const int hh = (slot & 3) ^ b_swz(col);
+    const int64_t c = min<int64_t>(n0 + col, p.N - 1);
+    o.b[j] = (uint32_t)(c * (p.K / 2) + hh * 16);
+  }
+  // element index (group 0) of the scale column this lane copies
+  const uint32_t os =
+      (uint32_t)(min<int64_t>(n0 + (wave % S_WAVES) * 64 + lane, p.N - 1) * p.G);
 
-  f32x4 acc[8][4];
+  f32x4 acc[8][JF];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < JF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // scales of the next group stay raw until after the barrier so that the
-  // loads overlap the current group's MFMAs
-  float scf[4];
-  uint16_t scn[4];
-  issue_stage(p, m0, n0, 0, sA0, sB0, sN0, wave, lane);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) scf[j] = f16_to_f32(srow[j][0]);
+  issue_stage(p, o, os, m0, 0, sA0, sB0, sN0, sS0, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-
   for (int g = 0; g < p.G; g += 2) {
     // stage 0 holds group g
-    if (g + 1 < p.G) {
-      issue_stage(p, m0, n0, g + 1, sA1, sB1, sN1, wave, lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) scn[j] = srow[j][g + 1];
-    }
-    compute_stage(sA0, sB0, sN0, scf, wave, lane, acc);
+    if (g + 1 < p.G) issue_stage(p, o, os, m0, g + 1, sA1, sB1, sN1, sS1, wave, lane);
+    compute_stage(sA0, sB0, sN0, sS0, wave, lane, acc);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (g + 1 >= p.G) break;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) scf[j] = f16_to_f32(scn[j]);
     // stage 1 holds group g + 1
-    if (g + 2 < p.G) {
-      issue_stage(p, m0, n0, g + 2, sA0, sB0, sN0, wave, lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) scn[j] = srow[j][g + 2];
-    }
-    compute_stage(sA1, sB1, sN1, scf, wave, lane, acc);
+    if (g + 2 < p.G) issue_stage(p, o, os, m0, g + 2, sA0, sB0, sN0, sS0, wave, lane);
+    compute_stage(sA1, sB1, sN1, sS1, wave, lane, acc);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) scf[j] = f16_to_f32(scn[j]);
   }
 
   store_tile<EPI>(p, m0, n0, wave, lane, acc);
 }
 
+template <int EPI>
+hipError_t launch_one(const GemmParams& p, hipStream_t s) {
+  const dim3 grid((unsigned)(p.tiles_m * p.tiles_n));
+  hipLaunchKernelGGL(k_gemm<EPI>, grid, dim3(NW * 64), 0, s, p);
+  return hipGetLastError();
+}
+
 }  // namespace
 
+// The kernels address operands with 32-bit byte offsets; larger problems are
+// split here into row / column chunks that each stay below 2^31 bytes.
 hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
                        int64_t K, int epilogue, hipStream_t s) {
-  GemmParams p;
-  p.xp = xp;
-  p.ns = ns;
-  p.qw = qw;
-  p.sc = sc;
-  p.out = out;
-  p.ldo = ldo;
-  p.Mp = Mp;
-  p.M = (int)M;
-  p.N = (int)N;
-  p.K = (int)K;
-  p.G = (int)(K / kGroup);
-  p.tiles_m = (int)((M + BM - 1) / BM);
-  p.tiles_n = (int)((N + BN - 1) / BN);
-  const dim3 grid((unsigned)(p.tiles_m * p.tiles_n));
-  switch (epilogue) {
-    case 1: hipLaunchKernelGGL(k_gemm<1>, grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL(k_gemm<2>, grid, dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL(k_gemm<0>, grid, dim3(256), 0, s, p); break;
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t mrows = std::max<int64_t>(BM, (lim / (K * 2)) / BM * BM);
+  const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
+  const size_t esize = epilogue == 2 ? 4 : 2;
+  for (int64_t m_s = 0; m_s < M; m_s += mrows) {
+    for (int64_t n_s = 0; n_s < N; n_s += ncols) {
+      GemmParams p;
+      p.xp = xp + m_s * K;
+      p.ns = ns + m_s;
+      p.qw = qw + n_s * (K / 2);
+      p.sc = sc + n_s * (K / kGroup);
+      p.out = static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize;
+      p.ldo = ldo;
+      p.Mp = Mp;
+      p.M = (int)std::min(mrows, M - m_s);
+      p.N = (int)std::min(ncols, N - n_s);
+      p.K = (int)K;
+      p.G = (int)(K / kGroup);
+      p.tiles_m = (p.M + BM - 1) / BM;
+      p.tiles_n = (p.N + BN - 1) / BN;
+      hipError_t e;
+      switch (epilogue) {
+        case 1: e = launch_one<1>(p, s); break;
+        case 2: e = launch_one<2>(p, s); break;
+        default: e = launch_one<0>(p, s); break;
+      }
+      if (e != hipSuccess) return e;
+    }
   }
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace ql
