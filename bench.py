@@ -32,10 +32,31 @@ PROJ = ("qkv", "out", "up", "down")
 # projection -> kernel symbol it launches (epilogue template argument)
 KERNEL_OF = {"qkv": "k_gemm<0> (bf16 store)", "out": "k_gemm<2> (fp32 residual add)",
              "up": "k_gemm<1> (GELU)", "down": "k_gemm<2> (fp32 residual add)"}
+SYMBOL = {v: v.split(" ")[0] for v in KERNEL_OF.values()}
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def measured_traffic(kernel_symbol: str):
+    """HBM bytes per launch of `kernel_symbol` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when the kernel sources have
+    changed since those counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in ("ql_gemm.hip", "ql_device.h", "ql_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_30877_amd", "csrc", f), "rb").read())
+    if rec.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    k = rec.get("kernels", {}).get(kernel_symbol)
+    return None if k is None else int(k["bytes_per_launch"])
 
 
 def build_stack(ql, synth, torch, L, d, dff):
@@ -136,7 +157,7 @@ def bench_stack(args, ql, synth, torch):
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "flops_per_launch": int(ff / nn), "launches": nn,
-                     "traffic": None},
+                     "traffic": measured_traffic(SYMBOL[sym]), "traffic_unit": "bytes/launch"},
         "kernels": kern,
         "gemm_share_of_step": round(gemm_ms / ms, 4),
         "weight_stream_GBps": round(L * sum(wbytes.values()) / (ms / 1e3) / 1e9, 1),
