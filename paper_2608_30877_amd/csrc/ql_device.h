@@ -44,15 +44,16 @@ __device__ __forceinline__ u32x4 permute_chunk(u32x4 v) {
 
 // 8 int4 codes (two's complement) -> 8 bf16 values equal to 136 + q, exactly:
 // u = q + 8 = nibble ^ 8 in [0, 15], and the bf16 pattern 0x4300 | u is
-// 128 + u.  The constant 136 is removed through the correction term that
-// starts every MFMA chain (-136 * sum of the activations of the group).
+// 128 + u.  Both steps fold into one mask and one XOR per dword,
+// ((w >> 4i) & 0x000F000F) ^ 0x43084308 (a single v_bitop3 on gfx950).  The
+// constant 136 is removed through the correction term that starts every
+// MFMA chain (-136 * sum of the activations of the group).
 __device__ __forceinline__ bf16x8 unpack_offset_codes(uint32_t w) {
-  const uint32_t u = w ^ 0x88888888u;
   u32x4 d;
-  d.x = (u & 0x000f000fu) | 0x43004300u;
-  d.y = ((u >> 4) & 0x000f000fu) | 0x43004300u;
-  d.z = ((u >> 8) & 0x000f000fu) | 0x43004300u;
-  d.w = ((u >> 12) & 0x000f000fu) | 0x43004300u;
+  d.x = (w & 0x000f000fu) ^ 0x43084308u;
+  d.y = ((w >> 4) & 0x000f000fu) ^ 0x43084308u;
+  d.z = ((w >> 8) & 0x000f000fu) ^ 0x43084308u;
+  d.w = ((w >> 12) & 0x000f000fu) ^ 0x43084308u;
   return __builtin_bit_cast(bf16x8, d);
 }
 

@@ -7,16 +7,17 @@
 // 128-wide scale group per step:
 //   * the activation tile (128 rows x 128 k, pre-permuted bf16), the packed
 //     weight tile (256 columns x 64 bytes), the group's 256 scales and 128
-//     correction terms are copied global -> LDS with direct-to-LDS loads,
-//     double-buffered, one group ahead (no register holds in-flight data, so
-//     no wait is needed before the end of the step);
+//     correction terms are copied global -> LDS with direct-to-LDS loads into
+//     a three-stage ring: while group g is computed, the copies of groups
+//     g+1 and g+2 are in flight, so each copy has about two steps to land;
 //   * each wave unpacks its 32 x 128 int4 codes once into bf16 values
 //     136 + q (exact; see unpack_offset_codes) and reuses them for all 8
 //     row fragments;
 //   * per 16 x 16 output fragment, a chain of four 16x16x32 MFMAs covers the
 //     group.  The chain starts from the correction -136 * sum_k x[m][k], so
 //     its result is the integer-code dot product sum x*q (fp32), and one fp32
-//     FMA applies the group's scale: acc += chain * s[n][g].
+//     FMA applies the group's scale: acc += chain * s[n][g].  That FMA is
+//     issued one fragment later, so it never waits on the chain's last MFMA.
 // Scales therefore stay exact fp32 (no bf16 rounding of q*s).
 #include <algorithm>
 
@@ -36,8 +37,15 @@ constexpr int A_SLOTS = BM * 16;       // 16-byte slots per stage (32 KB)
 constexpr int B_SLOTS = BN * 4;        // 16 KB
 constexpr int A_PER_WAVE = A_SLOTS / 64 / NW;   // 4 direct-to-LDS loads per wave
 constexpr int B_PER_WAVE = B_SLOTS / 64 / NW;   // 2
-constexpr int S_WAVES = BN / 64;                // waves that copy the scales
 static_assert(BN == kGemmBN, "tile width");
+// Copies each wave issues per group after its single correction / scale copy
+// (see issue_stage); waiting until at most this many are outstanding means
+// every copy of the group before has landed.
+constexpr int kLaterCopies = A_PER_WAVE + B_PER_WAVE;
+static_assert(kLaterCopies < 16, "vmcnt immediate");
+// s_waitcnt immediate (gfx9 layout): vmcnt(kLaterCopies), lgkmcnt(0), expcnt
+// not waited on
+constexpr int kWaitPrevGroup = 0x0070 | kLaterCopies;
 
 struct GemmParams {
   const uint16_t* xp;
@@ -63,30 +71,66 @@ __device__ __forceinline__ int a_msk(int row) {
 __device__ __forceinline__ int a_phys(int row, int chunk) { return chunk ^ a_msk(row); }
 __device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2)) & 3; }
 
+// Direct-to-LDS copy of BYTES per lane: lane l writes lds + l * BYTES (a
+// 2-byte copy writes its value zero-extended into the dword lds + 4 * l).
+// Written as inline assembly so that the compiler does not track these loads:
+// its own wait insertion cannot tell the three ring stages apart and would
+// wait for the copies just issued before every LDS read.  The kernel waits
+// for them explicitly (kWaitPrevGroup before the step barrier, vmcnt(0)
+// before the epilogue), and issues no other vector memory load in its loop.
+// M0 carries the LDS base; one wait state must separate its write from the
+// load that reads it.
+template <int BYTES>
+__device__ __forceinline__ void copy_to_lds(const void* src, const void* lds) {
+  const uint32_t l = (uint32_t)reinterpret_cast<uintptr_t>(lds);
+  if constexpr (BYTES == 16) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(src), "s"(l) : "memory", "m0");
+  } else if constexpr (BYTES == 4) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :: "v"(src), "s"(l) : "memory", "m0");
+  } else {
+    static_assert(BYTES == 2, "copy width");
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_ushort %0, off"
+                 :: "v"(src), "s"(l) : "memory", "m0");
+  }
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// also wait for every copy in flight).
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+struct Stage {
+  u32x4* A;     // activation tile, A_SLOTS 16-byte slots
+  u32x4* B;     // code tile, B_SLOTS 16-byte slots
+  float* N;     // BM correction terms
+  uint32_t* S;  // BN scales, one zero-extended binary16 per dword
+};
+
 struct Offsets {
   uint32_t a[A_PER_WAVE];  // byte offsets into xp of this lane's A slots (group 0)
   uint32_t b[B_PER_WAVE];  // byte offsets into qw of this lane's B slots (group 0)
 };
 
+// Copies of group g into stage st.  Waves 0-1 copy the 128 correction terms,
+// waves 2-5 the 256 scales, each first; then every wave issues kLaterCopies
+// activation / code copies.
 __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets& o, uint32_t os,
-                                            int64_t m0, int g, u32x4* sA, u32x4* sB, float* sN,
-                                            uint32_t* sS, int wave, int lane) {
+                                            int64_t m0, int g, const Stage& st, int wave, int lane) {
   const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
   const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
+  if (wave < 2)
+    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + wave * 64 + lane, st.N + wave * 64);
+  else if (wave < 6)
+    copy_to_lds<2>(p.sc + os + g, st.S + (wave - 2) * 64);
 #pragma unroll
-  for (int j = 0; j < A_PER_WAVE; ++j)
-    __builtin_amdgcn_global_load_lds(xa + o.a[j], sA + (j * NW + wave) * 64, 16, 0, 0);
+  for (int j = 0; j < A_PER_WAVE; ++j) copy_to_lds<16>(xa + o.a[j], st.A + (j * NW + wave) * 64);
 #pragma unroll
-  for (int j = 0; j < B_PER_WAVE; ++j)
-    __builtin_amdgcn_global_load_lds(qb + o.b[j], sB + (j * NW + wave) * 64, 16, 0, 0);
-  if (wave == 0) {
-    const float* src = p.ns + (size_t)g * p.Mp + m0 + lane;
-    __builtin_amdgcn_global_load_lds(src, sN, 4, 0, 0);
-    __builtin_amdgcn_global_load_lds(src + 64, sN + 64, 4, 0, 0);
-  }
-  // scales: a 2-byte direct-to-LDS copy lands zero-extended in one dword per
-  // lane; wave w < S_WAVES copies columns [64w, 64w+64) of the tile
-  if (wave < S_WAVES) __builtin_amdgcn_global_load_lds(p.sc + os + g, sS + wave * 64, 2, 0, 0);
+  for (int j = 0; j < B_PER_WAVE; ++j) copy_to_lds<16>(qb + o.b[j], st.B + (j * NW + wave) * 64);
 }
 
 template <int EPI>
@@ -117,37 +161,53 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
   }
 }
 
-__device__ __forceinline__ void load_a(const u32x4* sA, const float* sN, int i, int h, int lr,
-                                       bf16x8 (&a)[4], f32x4& n4) {
+__device__ __forceinline__ void load_a(const Stage& st, int i, int h, int lr, bf16x8 (&a)[4],
+                                       f32x4& n4) {
   const int row = i * 16 + lr;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(sA[row * 16 + a_phys(row, h * 4 + s)]);
-  n4 = *reinterpret_cast<const f32x4*>(sN + i * 16 + h * 4);
+  for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
+  n4 = *reinterpret_cast<const f32x4*>(st.N + i * 16 + h * 4);
 }
 
-__device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, const float* sN,
-                                              const uint32_t* sS, int wave, int lane,
-                                              f32x4 (&acc)[8][JF]) {
-  const int h = lane >> 4, lr = lane & 15;
-  float scf[JF];
-#pragma unroll
-  for (int j = 0; j < JF; ++j) scf[j] = f16_to_f32((uint16_t)sS[wave * WN + j * 16 + lr]);
-  bf16x8 a[4], an[4];
-  f32x4 n4, nn;
-  load_a(sA, sN, 0, h, lr, a, n4);
-  bf16x8 bq[JF][4];
+__device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
+                                       bf16x8 (&bq)[JF][4]) {
 #pragma unroll
   for (int j = 0; j < JF; ++j) {
     const int col = wave * WN + j * 16 + lr;
-    const u32x4 raw = sB[col * 4 + (h ^ b_swz(col))];
+    const u32x4 raw = st.B[col * 4 + (h ^ b_swz(col))];
     bq[j][0] = unpack_offset_codes(raw.x);
     bq[j][1] = unpack_offset_codes(raw.y);
     bq[j][2] = unpack_offset_codes(raw.z);
     bq[j][3] = unpack_offset_codes(raw.w);
   }
+}
+
+// One group.  On entry bq holds the group's unpacked codes and (a, n4) its
+// row fragment 0; fragment i + 1 is read from LDS during fragment i's MFMAs.
+// The scale FMAs of fragment i are issued during fragment i + 1; those of
+// fragment 7 are carried in (cprev, sprev) into the next group.  Before the
+// last fragment every read of `cur` is complete, so the wave waits for its
+// copies of the next group and joins the step barrier; the next group's
+// codes and fragment 0 are then read from `nxt` under fragment 7's MFMAs.
+__device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt, int wave,
+                                              int lane, bf16x8 (&bq)[JF][4], bf16x8 (&a)[4],
+                                              f32x4& n4, f32x4 (&cprev)[JF], float (&sprev)[JF],
+                                              f32x4 (&acc)[8][JF]) {
+  const int h = lane >> 4, lr = lane & 15;
+  float scf[JF];
+#pragma unroll
+  for (int j = 0; j < JF; ++j) scf[j] = f16_to_f32((uint16_t)cur.S[wave * WN + j * 16 + lr]);
+  bf16x8 an[4];
+  f32x4 nn;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    if (i + 1 < 8) load_a(sA, sN, i + 1, h, lr, an, nn);
+    if (i + 1 < 8) {
+      load_a(cur, i + 1, h, lr, an, nn);
+    } else {
+      __builtin_amdgcn_s_waitcnt(kWaitPrevGroup);
+      wg_barrier();
+      load_a(nxt, 0, h, lr, an, nn);
+    }
     f32x4 c[JF];
 #pragma unroll
     for (int j = 0; j < JF; ++j) c[j] = n4;
@@ -157,12 +217,16 @@ __device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, 
       for (int j = 0; j < JF; ++j) c[j] = mfma16x16x32(a[s], bq[j][s], c[j]);
     }
 #pragma unroll
-    for (int j = 0; j < JF; ++j) acc[i][j] += c[j] * scf[j];
-    if (i + 1 < 8) {
+    for (int j = 0; j < JF; ++j) acc[(i + 7) & 7][j] += cprev[j] * sprev[j];
+    if (i == 7) load_b(nxt, wave, h, lr, bq);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) a[s] = an[s];
-      n4 = nn;
+    for (int j = 0; j < JF; ++j) {
+      cprev[j] = c[j];
+      sprev[j] = scf[j];
     }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) a[s] = an[s];
+    n4 = nn;
     // keep the row fragments in program order: hoisting later fragments'
     // LDS reads above this point would only raise register pressure
     __builtin_amdgcn_sched_barrier(0);
@@ -171,17 +235,14 @@ __device__ __forceinline__ void compute_stage(const u32x4* sA, const u32x4* sB, 
 
 template <int EPI>
 __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
-  __shared__ u32x4 sA0[A_SLOTS];
-  __shared__ u32x4 sA1[A_SLOTS];
-  __shared__ u32x4 sB0[B_SLOTS];
-  __shared__ u32x4 sB1[B_SLOTS];
-  __shared__ float sN0[BM];
-  __shared__ float sN1[BM];
-  __shared__ uint32_t sS0[BN];
-  __shared__ uint32_t sS1[BN];
+  __shared__ u32x4 sA0[A_SLOTS], sA1[A_SLOTS], sA2[A_SLOTS];
+  __shared__ u32x4 sB0[B_SLOTS], sB1[B_SLOTS], sB2[B_SLOTS];
+  __shared__ float sN0[BM], sN1[BM], sN2[BM];
+  __shared__ uint32_t sS0[BN], sS1[BN], sS2[BN];
+  const Stage S0{sA0, sB0, sN0, sS0}, S1{sA1, sB1, sN1, sS1}, S2{sA2, sB2, sN2, sS2};
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63, lr = lane & 15;
+  const int lane = threadIdx.x & 63, lr = lane & 15, h = lane >> 4;
 
   // workgroup -> tile: first spread consecutive tiles over the 8 XCDs'
   // dispatch order so that each XCD sees a contiguous tile range, then walk
@@ -219,9 +280,9 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     const int64_t c = min<int64_t>(n0 + col, p.N - 1);
     o.b[j] = (uint32_t)(c * (p.K / 2) + hh * 16);
   }
-  // element index (group 0) of the scale column this lane copies
+  // element index (group 0) of the scale column this lane copies (waves 2-5)
   const uint32_t os =
-      (uint32_t)(min<int64_t>(n0 + (wave % S_WAVES) * 64 + lane, p.N - 1) * p.G);
+      (uint32_t)(min<int64_t>(n0 + ((wave - 2) & 3) * 64 + lane, p.N - 1) * p.G);
 
   f32x4 acc[8][JF];
 #pragma unroll
@@ -229,22 +290,42 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < JF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  issue_stage(p, o, os, m0, 0, sA0, sB0, sN0, sS0, wave, lane);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int g = 0; g < p.G; g += 2) {
-    // stage 0 holds group g
-    if (g + 1 < p.G) issue_stage(p, o, os, m0, g + 1, sA1, sB1, sN1, sS1, wave, lane);
-    compute_stage(sA0, sB0, sN0, sS0, wave, lane, acc);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (g + 1 >= p.G) break;
-    // stage 1 holds group g + 1
-    if (g + 2 < p.G) issue_stage(p, o, os, m0, g + 2, sA0, sB0, sN0, sS0, wave, lane);
-    compute_stage(sA1, sB1, sN1, sS1, wave, lane, acc);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  // group g lives in stage g % 3; step g issues group g + 2, clamped to the
+  // last group so that every step issues the same copies (the surplus ones
+  // land in a stage that is not read again)
+  const int G = p.G, Gl = p.G - 1;
+  issue_stage(p, o, os, m0, 0, S0, wave, lane);
+  issue_stage(p, o, os, m0, min(1, Gl), S1, wave, lane);
+  __builtin_amdgcn_s_waitcnt(kWaitPrevGroup);
+  wg_barrier();
+
+  bf16x8 bq[JF][4], a[4];
+  f32x4 n4;
+  f32x4 cprev[JF];  // carried chain of the last fragment; starts as 0 * 0
+  float sprev[JF];
+#pragma unroll
+  for (int j = 0; j < JF; ++j) {
+    cprev[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    sprev[j] = 0.f;
   }
+  load_b(S0, wave, h, lr, bq);
+  load_a(S0, 0, h, lr, a, n4);
+  int g = 0;
+  for (;;) {
+    issue_stage(p, o, os, m0, min(g + 2, Gl), S2, wave, lane);
+    compute_stage(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
+    if (++g >= G) break;
+    issue_stage(p, o, os, m0, min(g + 2, Gl), S0, wave, lane);
+    compute_stage(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
+    if (++g >= G) break;
+    issue_stage(p, o, os, m0, min(g + 2, Gl), S1, wave, lane);
+    compute_stage(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
+    if (++g >= G) break;
+  }
+  // no copy may still be writing LDS when the workgroup retires
+  __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+  for (int j = 0; j < JF; ++j) acc[7][j] += cprev[j] * sprev[j];
 
   store_tile<EPI>(p, m0, n0, wave, lane, acc);
 }
