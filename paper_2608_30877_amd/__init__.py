@@ -96,6 +96,8 @@ def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
         raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
     if ndim is not None and t.dim() != ndim:
         raise ValueError(f"{name} must be {ndim}-D")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
 
 
 _BITS16 = (torch.bfloat16, torch.int16, torch.uint16, torch.float16)

@@ -27,7 +27,7 @@ int check_shape(int64_t M, int64_t N, int64_t K, int32_t group) {
 inline int hip_status(hipError_t e) { return e == hipSuccess ? QL_OK : QL_ERR_HIP; }
 
 size_t forward_ws_bytes(int64_t M, int64_t K) {
-  if (M <= kSmallM) return 0;
+  if (use_gemv(M, K)) return 0;
   return xp_bytes(M, K) + ns_bytes(M, K);
 }
 
@@ -35,7 +35,7 @@ size_t forward_ws_bytes(int64_t M, int64_t K) {
 int run_linear(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc, void* out,
                int64_t ldo, int64_t M, int64_t N, int64_t K, int epi, void* ws,
                hipStream_t s) {
-  if (M <= kSmallM) return hip_status(launch_gemv(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
+  if (use_gemv(M, K)) return hip_status(launch_gemv(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
   uint16_t* xp = static_cast<uint16_t*>(ws);
   float* ns = reinterpret_cast<float*>(static_cast<char*>(ws) + xp_bytes(M, K));
   const int64_t Mp = padded_rows(M);
@@ -78,11 +78,13 @@ int owned_workspace(hipStream_t s, size_t need, void** out) {
 
 // ---- stack workspace layout
 struct StackLayout {
+  bool small;  // every projection runs the small-batch kernel
   size_t a, qkv, u, up, ns, total;
 };
 
 StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   StackLayout L;
+  L.small = use_gemv(M, d) && use_gemv(M, d_ff);
   size_t off = 0;
   L.a = off;
   off += align256((size_t)M * d * 2);
@@ -91,10 +93,10 @@ StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   L.u = off;
   off += align256((size_t)M * d_ff * 2);
   L.up = off;
-  off += (M > kSmallM) ? align256((size_t)M * d_ff * 2) : 0;
+  off += L.small ? 0 : align256((size_t)M * d_ff * 2);
   L.ns = off;
   const int64_t kmax = d_ff > d ? d_ff : d;
-  off += (M > kSmallM) ? ns_bytes(M, kmax) : 0;
+  off += L.small ? 0 : ns_bytes(M, kmax);
   L.total = off;
   return L;
 }
@@ -228,7 +230,7 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
   uint16_t* up = reinterpret_cast<uint16_t*>(ws + L.up);
   float* ns = reinterpret_cast<float*>(ws + L.ns);
   const int64_t Mp = padded_rows(M);
-  const bool small = M <= kSmallM;
+  const bool small = L.small;
   hipError_t e = hipSuccess;
 #define QL_TRY(call)               \
   do {                             \

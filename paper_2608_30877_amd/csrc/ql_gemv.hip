@@ -3,19 +3,31 @@
 // Each workgroup (4 waves) owns 64 output columns over the full K; wave w
 // takes the scale groups g = w, w+4, w+8, ... so the four waves stream
 // adjacent 64-byte pieces of the same weight rows.  Per group, each lane
-// issues one 16-byte load per 16-column fragment (the lane's 32 codes),
-// unpacks them to bf16 136 + q and runs a 16x16x32 MFMA chain against the
-// (at most 16) activation rows; the activation rows' group sums come from
-// one more MFMA chain against a constant -136 operand, which starts each
-// chain so that it yields the exact code dot product.  The partial sums of
-// the four waves are then reduced through LDS (the wavefront reduction) and
-// the epilogue is applied.
+// issues one 16-byte load per 16-column fragment (the lane's 32 codes) and
+// four for its activation row; these loads are unconditional (indices past
+// the last group are clamped) and kept two groups deep in registers, so the
+// compiler's counted waits let the next group's loads fly while the current
+// one is computed.  The codes are unpacked to bf16 136 + q and run through a
+// 16x16x32 MFMA chain against the (at most 16) activation rows; the rows'
+// group sums come from one more MFMA chain against a constant -136 operand,
+// which starts each chain so that it yields the exact code dot product.  The
+// workgroup's scales (64 columns x G, one contiguous block of the scale
+// matrix) are copied into LDS once at the start: per-group scale loads would
+// cost as many memory instructions as the codes themselves.  The partial
+// sums of the four waves are then reduced through LDS (the wavefront
+// reduction) and the epilogue is applied.
+#include <algorithm>
+
 #include "ql_device.h"
 #include "ql_internal.h"
 
 namespace ql {
 
 namespace {
+
+constexpr int kWaves = 4;
+constexpr int kDepth = 2;   // groups of loads in flight per wave
+constexpr int kCols = 64;   // output columns per workgroup
 
 struct GemvParams {
   const uint16_t* x;
@@ -27,25 +39,22 @@ struct GemvParams {
 };
 
 struct GroupData {
-  u32x4 b[4];
-  uint16_t s[4];
-  u32x4 a[4];
+  u32x4 b[4];  // codes of the 4 column fragments
+  u32x4 a[4];  // activations, 4 k-steps of 8
 };
 
-__device__ __forceinline__ void load_group(const GemvParams& p, const uint8_t* const (&wrow)[4],
-                                           const uint16_t* const (&srow)[4], const uint16_t* xrow,
+__device__ __forceinline__ void load_group(const uint8_t* const (&wrow)[4], const uint16_t* xrow,
                                            int g, int h, GroupData& d) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 4; ++j)
     d.b[j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)g * (kGroup / 2));
-    d.s[j] = srow[j][g];
-  }
 #pragma unroll
   for (int s = 0; s < 4; ++s)
     d.a[s] = *reinterpret_cast<const u32x4*>(xrow + (int64_t)g * kGroup + (h * 4 + s) * 8);
 }
 
-__device__ __forceinline__ void compute_group(const GroupData& d, f32x4 (&acc)[4]) {
+__device__ __forceinline__ void compute_group(const GroupData& d, const uint16_t* sS, int G, int g,
+                                              int lr, f32x4 (&acc)[4]) {
   const bf16x8 neg = neg136x8();
   bf16x8 a[4];
 #pragma unroll
@@ -63,56 +72,104 @@ __device__ __forceinline__ void compute_group(const GroupData& d, f32x4 (&acc)[4
     }
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] += c[j] * f16_to_f32(d.s[j]);
+  for (int j = 0; j < 4; ++j) acc[j] += c[j] * f16_to_f32(sS[(j * 16 + lr) * G + g]);
+}
+
+// Copy `count` binary16 values from src to LDS dst with all of a thread's
+// loads of a batch in flight together (16-byte loads when src is 16-byte
+// aligned, which also makes dst's 16-byte slots line up).
+__device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, int count) {
+  const int t = threadIdx.x, nt = kWaves * 64;
+  int done = 0;
+  if (((uintptr_t)src & 15u) == 0) {
+    const int nv = count / 8;
+    const u32x4* s = reinterpret_cast<const u32x4*>(src);
+    u32x4* d = reinterpret_cast<u32x4*>(dst);
+    for (int v0 = 0; v0 < nv; v0 += 4 * nt) {
+      u32x4 r[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = v0 + u * nt + t;
+        if (v < nv) r[u] = s[v];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = v0 + u * nt + t;
+        if (v < nv) d[v] = r[u];
+      }
+    }
+    done = nv * 8;
+  }
+  for (int i0 = done; i0 < count; i0 += 8 * nt) {
+    uint16_t r[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * nt + t;
+      if (i < count) r[u] = src[i];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * nt + t;
+      if (i < count) dst[i] = r[u];
+    }
+  }
 }
 
 template <int EPI>
-__global__ __launch_bounds__(256) void k_gemv(GemvParams p) {
-  __shared__ f32x4 red[3][4][64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+__global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
+  // [kWaves-1][4][64] partial sums, then the scales [kCols][G]
+  extern __shared__ __align__(16) unsigned char smem[];
+  f32x4* red = reinterpret_cast<f32x4*>(smem);
+  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + (kWaves - 1) * 4 * 64 * sizeof(f32x4));
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = lane >> 4, lr = lane & 15;
-  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  const int64_t n0 = (int64_t)blockIdx.x * kCols;
+  const int G = p.G;
 
   // rows past M and columns past N read valid (clamped) memory; their
-  // results are never stored
+  // results are never stored (nor are the columns whose scales the
+  // workgroup's copy leaves unset)
   const uint16_t* xrow = p.x + (int64_t)min(lr, p.M - 1) * p.ldx;
   const uint8_t* wrow[4];
-  const uint16_t* srow[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int64_t col = min<int64_t>(n0 + j * 16 + lr, p.N - 1);
+    const int64_t col = std::min<int64_t>(n0 + j * 16 + lr, p.N - 1);
     wrow[j] = p.qw + col * (p.K / 2) + h * 16;
-    srow[j] = p.sc + col * p.G;
   }
 
   f32x4 acc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // software pipeline: the loads of the next group are in flight while the
-  // current one is unpacked and multiplied
-  int g = wave;
-  GroupData cur, nxt;
-  if (g < p.G) load_group(p, wrow, srow, xrow, g, h, cur);
-  while (g < p.G) {
-    const int gn = g + 4;
-    if (gn < p.G) load_group(p, wrow, srow, xrow, gn, h, nxt);
-    compute_group(cur, acc);
-    cur = nxt;
-    g = gn;
+  // groups of this wave: g = wave + kWaves * t, t < T; the loads of groups
+  // t + 1 .. t + kDepth - 1 are in flight while group t is computed
+  const int T = G > wave ? (G - wave + kWaves - 1) / kWaves : 0;
+  GroupData buf[kDepth];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) load_group(wrow, xrow, min(wave + kWaves * d, G - 1), h, buf[d]);
+  const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
+  copy_scales(p.sc + n0 * G, sS, cols * G);
+  __syncthreads();
+
+  for (int t0 = 0; t0 < T; t0 += kDepth) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      const int t = t0 + d;
+      if (t < T) compute_group(buf[d], sS, G, wave + kWaves * t, lr, acc);
+      load_group(wrow, xrow, min(wave + kWaves * (t + kDepth), G - 1), h, buf[d]);
+    }
   }
 
   if (wave > 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) red[wave - 1][j][lane] = acc[j];
+    for (int j = 0; j < 4; ++j) red[((wave - 1) * 4 + j) * 64 + lane] = acc[j];
   }
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
-  for (int w = 0; w < 3; ++w)
+  for (int w = 0; w < kWaves - 1; ++w)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] += red[w][j][lane];
-
+    for (int j = 0; j < 4; ++j) acc[j] += red[(w * 4 + j) * 64 + lane];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t col = n0 + j * 16 + lr;
@@ -136,6 +193,10 @@ __global__ __launch_bounds__(256) void k_gemv(GemvParams p) {
 
 }  // namespace
 
+size_t gemv_lds_bytes(int64_t K) {
+  return (size_t)(kWaves - 1) * 4 * 64 * sizeof(f32x4) + (size_t)kCols * (K / kGroup) * 2;
+}
+
 hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
                        void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
                        hipStream_t s) {
@@ -150,11 +211,12 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   p.N = (int)N;
   p.K = (int)K;
   p.G = (int)(K / kGroup);
-  const dim3 grid((unsigned)((N + 63) / 64));
+  const size_t lds = gemv_lds_bytes(K);
+  const dim3 grid((unsigned)((N + kCols - 1) / kCols)), block(kWaves * 64);
   switch (epilogue) {
-    case 1: hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL(k_gemv<0>, grid, dim3(256), 0, s, p); break;
+    case 1: hipLaunchKernelGGL(k_gemv<1>, grid, block, lds, s, p); break;
+    case 2: hipLaunchKernelGGL(k_gemv<2>, grid, block, lds, s, p); break;
+    default: hipLaunchKernelGGL(k_gemv<0>, grid, block, lds, s, p); break;
   }
   return hipGetLastError();
 }

@@ -47,7 +47,14 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
                        int64_t K, int epilogue, hipStream_t s);
 
-// Small-M kernel on raw bf16 activations (M <= kSmallM).
+// Small-M kernel on raw bf16 activations (M <= kSmallM).  It keeps the
+// workgroup's scales in LDS: gemv_lds_bytes(K) must stay within kGemvMaxLds
+// (K <= 53248); use_gemv picks it for the shapes it serves.
+constexpr size_t kGemvMaxLds = 65536;
+size_t gemv_lds_bytes(int64_t K);
+inline bool use_gemv(int64_t M, int64_t K) {
+  return M <= kSmallM && gemv_lds_bytes(K) <= kGemvMaxLds;
+}
 hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
                        void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
                        hipStream_t s);

@@ -104,6 +104,9 @@ def test_dequant_bit_exact(ql, N, K):
 SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel, ragged tails
     (1, 64, 128), (5, 250, 384), (8, 512, 512), (16, 512, 512), (16, 1000, 1280),
     (17, 256, 256), (64, 384, 512), (128, 256, 512), (200, 500, 640), (300, 1024, 1152),
+    # the largest K whose scales the small-batch kernel keeps in LDS, and the
+    # next group up, which a small batch runs on the MFMA kernel instead
+    (3, 70, 53248), (8, 96, 53376),
 ]
 
 
@@ -131,6 +134,24 @@ def test_forward_workload_inputs(ql, M, N, K):
     qw, sc = O.quantize_pack(synth.weights_f32(N + 13 * M, N, K))
     y = bf16_as_f64(_forward_np(ql, x, qw, sc))
     assert O.rel_fro(y, O.qlinear_ref(x, qw, sc)) <= TOL
+
+
+def test_small_batch_unaligned_scales(ql):
+    """Scales only 2-byte aligned: the small-batch kernel copies them to LDS
+    element by element instead of in 16-byte pieces."""
+    M, N, K = 8, 200, 1280
+    say(f"unaligned scales M={M} N={N} K={K}")
+    x = synth.ternary_bf16(5, M, K)
+    qw = synth.random_packed_bytes(6, N, K)
+    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
+    buf = torch.zeros(N * (K // 128) + 8, dtype=torch.int16, device="cuda")
+    sc_view = buf[1:1 + N * (K // 128)].view(N, K // 128)
+    sc_view.copy_(dev_u16(sc))
+    assert sc_view.data_ptr() % 16 == 2
+    y = ql.forward(dev_u16(x), dev(qw), sc_view)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_u16(y), ref)
 
 
 def test_forward_toy_config(ql):
