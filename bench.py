@@ -39,24 +39,36 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_traffic(kernel_symbol: str):
-    """HBM bytes per launch of `kernel_symbol` from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary, or None when the kernel sources have
-    changed since those counters were taken."""
+# source files each kernel family is built from
+KERNEL_SOURCES = {"k_gemm": ("ql_gemm.hip", "ql_device.h", "ql_internal.h"),
+                  "k_gemv": ("ql_gemv.hip", "ql_device.h", "ql_internal.h")}
+
+
+def sources_sha256(family: str) -> str:
     import hashlib
 
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[family]:
+        h.update(open(os.path.join(ROOT, "paper_2608_30877_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel_symbol: str):
+    """HBM bytes per launch of `kernel_symbol` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when the kernel's sources have
+    changed since those counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    h = hashlib.sha256()
-    for f in ("ql_gemm.hip", "ql_device.h", "ql_internal.h"):
-        h.update(open(os.path.join(ROOT, "paper_2608_30877_amd", "csrc", f), "rb").read())
-    if rec.get("kernel_source_sha256") != h.hexdigest():
-        return None
     k = rec.get("kernels", {}).get(kernel_symbol)
-    return None if k is None else int(k["bytes_per_launch"])
+    if k is None:
+        return None
+    family = kernel_symbol.split("<")[0]
+    if family not in KERNEL_SOURCES or k.get("source_sha256") != sources_sha256(family):
+        return None
+    return int(k["bytes_per_launch"])
 
 
 def build_stack(ql, synth, torch, L, d, dff):
@@ -191,7 +203,8 @@ def bench_small_batch(ql, synth, torch, reps=50, copies=4):
     return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0>", "avg_us": round(t * 1e6, 2),
             "weight_GBps": round(wb / t / 1e9, 1),
             "frac_hbm_peak": round(wb / t / 1e9 / PEAK_HBM_GBS, 4),
-            "algorithmic_bytes": int(wb + 2 * M * K + 2 * M * N)}
+            "algorithmic_bytes": int(wb + 2 * M * K + 2 * M * N),
+            "traffic": measured_traffic("k_gemv<0>"), "traffic_unit": "bytes/launch"}
 
 
 def bench_prefill(ql, synth, torch, reps=10):
