@@ -3,11 +3,13 @@
 // Each workgroup (4 waves) owns 64 output columns over the full K; wave w
 // takes the scale groups g = w, w+4, w+8, ... so the four waves stream
 // adjacent 64-byte pieces of the same weight rows.  Per group, each lane
-// issues one 16-byte load per 16-column fragment (the lane's 32 codes) and
-// four for its activation row; these loads are unconditional (indices past
-// the last group are clamped) and kept two groups deep in registers, so the
-// compiler's counted waits let the next group's loads fly while the current
-// one is computed.  The codes are unpacked to bf16 136 + q and run through a
+// issues one 16-byte load per 16-column fragment (the lane's 32 codes); the
+// group's activations (M rows x 256 bytes) come in ceil(M/4) contiguous
+// loads of 4 rows each and reach the MFMA operand layout through a
+// wave-private LDS tile, which costs far less than four 16-row loads in that
+// layout.  All loads are unconditional (indices past the last group are
+// clamped) and kept two groups deep in registers, so the compiler's counted
+// waits let the next group's loads fly while the current one is computed.  The codes are unpacked to bf16 136 + q and run through a
 // 16x16x32 MFMA chain against the (at most 16) activation rows; the rows'
 // group sums come from one more MFMA chain against a constant -136 operand,
 // which starts each chain so that it yields the exact code dot product.  The
@@ -28,6 +30,9 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kDepth = 2;   // groups of loads in flight per wave
 constexpr int kCols = 64;   // output columns per workgroup
+// LDS ahead of the scales: the waves' activation tiles, later the partial sums
+constexpr int kGemvTileBytes = kWaves * 256 * 16;
+static_assert((kWaves - 1) * 4 * 64 * 16 <= kGemvTileBytes, "partial sums fit the tiles");
 
 struct GemvParams {
   const uint16_t* x;
@@ -38,27 +43,45 @@ struct GemvParams {
   int M, N, K, G;
 };
 
+// Activation tile of one group in LDS: 16 rows x 16 chunks of 16 bytes, row r
+// storing chunk c at slot c ^ x_msk(r) so that the 16-row MFMA operand reads
+// are free of bank conflicts.
+__device__ __forceinline__ int x_msk(int row) {
+  row &= 15;
+  return row ^ ((((row >> 2) ^ (row >> 3)) & 1) << 2);
+}
+
+template <int XQ>
 struct GroupData {
-  u32x4 b[4];  // codes of the 4 column fragments
-  u32x4 a[4];  // activations, 4 k-steps of 8
+  u32x4 b[4];   // codes of the 4 column fragments
+  u32x4 a[XQ];  // activations: rows 4q + lane/16, chunk lane%16
 };
 
-__device__ __forceinline__ void load_group(const uint8_t* const (&wrow)[4], const uint16_t* xrow,
-                                           int g, int h, GroupData& d) {
+template <int XQ>
+__device__ __forceinline__ void load_group(const uint8_t* const (&wrow)[4],
+                                           const uint16_t* const (&xsrc)[XQ], int g,
+                                           GroupData<XQ>& d) {
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     d.b[j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)g * (kGroup / 2));
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
-    d.a[s] = *reinterpret_cast<const u32x4*>(xrow + (int64_t)g * kGroup + (h * 4 + s) * 8);
+  for (int q = 0; q < XQ; ++q)
+    d.a[q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)g * kGroup);
 }
 
-__device__ __forceinline__ void compute_group(const GroupData& d, const uint16_t* sS, int G, int g,
-                                              int lr, f32x4 (&acc)[4]) {
+template <int XQ>
+__device__ __forceinline__ void compute_group(const GroupData<XQ>& d, u32x4* xt,
+                                              const int (&xdst)[XQ], const uint16_t* sS, int G,
+                                              int g, int h, int lr, f32x4 (&acc)[4]) {
   const bf16x8 neg = neg136x8();
+  // through the wave's LDS tile into the operand layout (rows past M hold
+  // stale values; they only reach output rows that are never stored)
+#pragma unroll
+  for (int q = 0; q < XQ; ++q) xt[xdst[q]] = d.a[q];
   bf16x8 a[4];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(permute_chunk(d.a[s]));
+  for (int s = 0; s < 4; ++s)
+    a[s] = as_bf16x8(permute_chunk(xt[lr * 16 + ((h * 4 + s) ^ x_msk(lr))]));
   f32x4 nc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < 4; ++s) nc = mfma16x16x32(a[s], neg, nc);
@@ -115,12 +138,14 @@ __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, 
   }
 }
 
-template <int EPI>
+template <int EPI, int XQ>
 __global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
-  // [kWaves-1][4][64] partial sums, then the scales [kCols][G]
+  // [kWaves][256] activation tiles (after the loop: [kWaves-1][4][64] partial
+  // sums), then the scales [kCols][G]
   extern __shared__ __align__(16) unsigned char smem[];
+  u32x4* xtiles = reinterpret_cast<u32x4*>(smem);
   f32x4* red = reinterpret_cast<f32x4*>(smem);
-  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + (kWaves - 1) * 4 * 64 * sizeof(f32x4));
+  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + kGemvTileBytes);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = lane >> 4, lr = lane & 15;
   const int64_t n0 = (int64_t)blockIdx.x * kCols;
@@ -129,13 +154,21 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
   // rows past M and columns past N read valid (clamped) memory; their
   // results are never stored (nor are the columns whose scales the
   // workgroup's copy leaves unset)
-  const uint16_t* xrow = p.x + (int64_t)min(lr, p.M - 1) * p.ldx;
   const uint8_t* wrow[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t col = std::min<int64_t>(n0 + j * 16 + lr, p.N - 1);
     wrow[j] = p.qw + col * (p.K / 2) + h * 16;
   }
+  const uint16_t* xsrc[XQ];
+  int xdst[XQ];
+#pragma unroll
+  for (int q = 0; q < XQ; ++q) {
+    const int row = q * 4 + (lane >> 4), ch = lane & 15;
+    xsrc[q] = p.x + (int64_t)min(row, p.M - 1) * p.ldx + ch * 8;
+    xdst[q] = row * 16 + (ch ^ x_msk(row));
+  }
+  u32x4* xt = xtiles + wave * 256;
 
   f32x4 acc[4];
 #pragma unroll
@@ -144,9 +177,9 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
   // groups of this wave: g = wave + kWaves * t, t < T; the loads of groups
   // t + 1 .. t + kDepth - 1 are in flight while group t is computed
   const int T = G > wave ? (G - wave + kWaves - 1) / kWaves : 0;
-  GroupData buf[kDepth];
+  GroupData<XQ> buf[kDepth];
 #pragma unroll
-  for (int d = 0; d < kDepth; ++d) load_group(wrow, xrow, min(wave + kWaves * d, G - 1), h, buf[d]);
+  for (int d = 0; d < kDepth; ++d) load_group<XQ>(wrow, xsrc, min(wave + kWaves * d, G - 1), buf[d]);
   const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
   copy_scales(p.sc + n0 * G, sS, cols * G);
   __syncthreads();
@@ -155,11 +188,13 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
       const int t = t0 + d;
-      if (t < T) compute_group(buf[d], sS, G, wave + kWaves * t, lr, acc);
-      load_group(wrow, xrow, min(wave + kWaves * (t + kDepth), G - 1), h, buf[d]);
+      if (t < T) compute_group<XQ>(buf[d], xt, xdst, sS, G, wave + kWaves * t, h, lr, acc);
+      load_group<XQ>(wrow, xsrc, min(wave + kWaves * (t + kDepth), G - 1), buf[d]);
     }
   }
 
+  // the partial sums reuse the activation tiles' LDS
+  __syncthreads();
   if (wave > 0) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) red[((wave - 1) * 4 + j) * 64 + lane] = acc[j];
@@ -194,7 +229,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemv(GemvParams p) {
 }  // namespace
 
 size_t gemv_lds_bytes(int64_t K) {
-  return (size_t)(kWaves - 1) * 4 * 64 * sizeof(f32x4) + (size_t)kCols * (K / kGroup) * 2;
+  return (size_t)kGemvTileBytes + (size_t)kCols * (K / kGroup) * 2;
 }
 
 hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
@@ -213,11 +248,22 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   p.G = (int)(K / kGroup);
   const size_t lds = gemv_lds_bytes(K);
   const dim3 grid((unsigned)((N + kCols - 1) / kCols)), block(kWaves * 64);
-  switch (epilogue) {
-    case 1: hipLaunchKernelGGL(k_gemv<1>, grid, block, lds, s, p); break;
-    case 2: hipLaunchKernelGGL(k_gemv<2>, grid, block, lds, s, p); break;
-    default: hipLaunchKernelGGL(k_gemv<0>, grid, block, lds, s, p); break;
+  const int xq = (int)((M + 3) / 4);   // contiguous 4-row activation loads per group
+#define QL_GEMV(E, Q) hipLaunchKernelGGL((k_gemv<E, Q>), grid, block, lds, s, p)
+#define QL_GEMV_Q(E)                     \
+  switch (xq) {                          \
+    case 1: QL_GEMV(E, 1); break;        \
+    case 2: QL_GEMV(E, 2); break;        \
+    case 3: QL_GEMV(E, 3); break;        \
+    default: QL_GEMV(E, 4); break;       \
   }
+  switch (epilogue) {
+    case 1: QL_GEMV_Q(1); break;
+    case 2: QL_GEMV_Q(2); break;
+    default: QL_GEMV_Q(0); break;
+  }
+#undef QL_GEMV_Q
+#undef QL_GEMV
   return hipGetLastError();
 }
 

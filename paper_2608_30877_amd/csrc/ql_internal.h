@@ -49,7 +49,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
 
 // Small-M kernel on raw bf16 activations (M <= kSmallM).  It keeps the
 // workgroup's scales in LDS: gemv_lds_bytes(K) must stay within kGemvMaxLds
-// (K <= 53248); use_gemv picks it for the shapes it serves.
+// (K <= 49152); use_gemv picks it for the shapes it serves.
 constexpr size_t kGemvMaxLds = 65536;
 size_t gemv_lds_bytes(int64_t K);
 inline bool use_gemv(int64_t M, int64_t K) {

@@ -85,8 +85,8 @@ def test_forward_ex_errors_without_launch(lib):
     ws.argtypes = [i64, i64, i32]
     ws.restype = sz
     assert ws(16, 4096, 128) == 0                     # small-M path uses none
-    assert ws(16, 53248, 128) == 0                    # largest K it serves
-    assert ws(16, 53376, 128) > 0                     # beyond: MFMA path
+    assert ws(16, 49152, 128) == 0                    # largest K it serves
+    assert ws(16, 49280, 128) > 0                     # beyond: MFMA path
     assert ws(2048, 12288, 128) >= 2048 * 12288 * 2   # permuted activation copy
     assert ws(4, 100, 128) == 0                        # invalid shape -> 0
 

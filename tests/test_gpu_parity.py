@@ -106,7 +106,7 @@ SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel, ragged tails
     (17, 256, 256), (64, 384, 512), (128, 256, 512), (200, 500, 640), (300, 1024, 1152),
     # the largest K whose scales the small-batch kernel keeps in LDS, and the
     # next group up, which a small batch runs on the MFMA kernel instead
-    (3, 70, 53248), (8, 96, 53376),
+    (3, 70, 49152), (8, 96, 49280),
 ]
 
 
@@ -139,7 +139,7 @@ def test_forward_workload_inputs(ql, M, N, K):
 def test_small_batch_unaligned_scales(ql):
     """Scales only 2-byte aligned: the small-batch kernel copies them to LDS
     element by element instead of in 16-byte pieces."""
-    M, N, K = 8, 200, 1280
+    M, N, K = 11, 200, 1280
     say(f"unaligned scales M={M} N={N} K={K}")
     x = synth.ternary_bf16(5, M, K)
     qw = synth.random_packed_bytes(6, N, K)
