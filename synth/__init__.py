@@ -103,6 +103,27 @@ def weights_f32_cuda(seed: int, N: int, K: int, std: float = 0.02, out=None):
     return out
 
 
+def ternary_bf16_cuda(seed: int, M: int, K: int):
+    """x [M, K] with entries in {-1, 0, 1} as bf16 bit patterns (int16),
+    drawn on the current CUDA device with torch's seeded generator."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    t = torch.randint(-1, 2, (M, K), dtype=torch.int16, device="cuda", generator=g)
+    # bf16 bits of -1, 0, +1
+    return torch.where(t == 0, 0, torch.where(t > 0, 0x3F80, -16512)).to(torch.int16)
+
+
+def random_packed_bytes_cuda(seed: int, N: int, K: int):
+    """Uniform random code bytes [N, K/2] (uint8) on the current CUDA device."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    return torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+
+
 def random_scales_f16(seed: int, N: int, G: int, lo: float = 0.004, hi: float = 0.016) -> np.ndarray:
     """[N, G] binary16 bits of scales uniform in [lo, hi] (the range that
     N(0, 0.02) weights give), for packed weights drawn directly as bytes."""

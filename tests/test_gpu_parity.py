@@ -322,6 +322,37 @@ def test_full_exact_arithmetic_bit_exact(ql, M, N, K):
     np.testing.assert_array_equal(host_u16(y[:, ci]), ref)
 
 
+@pytest.mark.parametrize("M,N,K", [(90000, 256, 12288), (256, 360000, 12288)])
+def test_max_size_launch_split_bit_exact(ql, M, N, K):
+    """Operands past 2^31 bytes (activations 2.2 GB, or codes 2.2 GB): the
+    MFMA kernel's 32-bit offsets make the host split the launch into row /
+    column chunks.  Exact-arithmetic inputs drawn on the device, checked bit
+    for bit on rows or columns on both sides of the split."""
+    say(f"max-size split M={M} N={N} K={K}")
+    x = synth.ternary_bf16_cuda(31, M, K)
+    qw = synth.random_packed_bytes_cuda(32, N, K)
+    sc = dev_u16(synth.const_f16_bits(N, K // 128, 0x3000))
+    y = ql.forward(x, qw, sc)
+    torch.cuda.synchronize()
+    rows_lim = (2 ** 31 // (K * 2)) // 128 * 128      # row chunk of the split
+    cols_lim = (2 ** 31 // (K // 2)) // 256 * 256     # column chunk
+    rng = np.random.default_rng(M + N)
+    if M * K * 2 >= 2 ** 31:
+        rows = np.unique(np.r_[0, rows_lim - 1, rows_lim, M - 1, rng.integers(0, M, 12)])
+        cols = np.arange(N)
+    else:
+        rows = np.arange(M)
+        cols = np.unique(np.r_[0, cols_lim - 1, cols_lim, N - 1, rng.integers(0, N, 12)])
+    ri = torch.from_numpy(rows).cuda()
+    ci = torch.from_numpy(cols).cuda()
+    xs = host_u16(x[ri])
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(xs, qw[ci].cpu().numpy(),
+                                           synth.const_f16_bits(len(cols), K // 128, 0x3000)))
+    np.testing.assert_array_equal(host_u16(y[ri][:, ci]), ref)
+    del x, qw, y
+    torch.cuda.empty_cache()
+
+
 # ------------------------------------------------------------------ RMSNorm
 
 @pytest.mark.parametrize("M,d", [(3, 256), (64, 12288)])
