@@ -165,8 +165,12 @@ size_t qlayer_stack_workspace_bytes(int64_t M, int64_t d, int64_t d_ff,
  *              256-byte aligned.  Layout (byte offsets, each 256-aligned):
  *              [0]        a / a2 staging  bf16 [M][d]   (internal layout)
  *              [qkv_off]  qkv             bf16 [M][3d]  (row-major)
- *              [u_off]    u               bf16 [M][d_ff] (row-major)
- *              then the correction terms; see qlayer_stack_workspace_offsets.
+ *              [u_off]    u               bf16 [M][d_ff]: row-major when
+ *                         M <= 16; for larger M the MFMA operand layout,
+ *                         in which each 8-element chunk of a row holds
+ *                         elements (0,4,1,5,2,6,3,7) of that chunk
+ *              then, for M > 16, the prepared V copy and two correction-term
+ *              arrays; see qlayer_stack_workspace_offsets.
  *   d, d_ff    multiples of 128.
  */
 int qlayer_stack_forward(const ql_layer* layers, int32_t n_layers, float* h,

@@ -77,14 +77,20 @@ int owned_workspace(hipStream_t s, size_t need, void** out) {
 }
 
 // ---- stack workspace layout
+// Small batches run the row-major kernel chain: a, qkv, u.  Larger ones keep
+// every GEMM input in the MFMA operand layout: a (RMSNorm output, with ns0),
+// av (the V slice, written by the QKV epilogue with ns1) and u (the GELU
+// output, written by the up projection's epilogue with ns1).  No GEMM reads
+// and writes the same correction array.
 struct StackLayout {
   bool small;  // every projection runs the small-batch kernel
-  size_t a, qkv, u, up, ns, total;
+  size_t a, qkv, u, av, ns0, ns1, total;
 };
 
 StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   StackLayout L;
   L.small = use_gemv(M, d) && use_gemv(M, d_ff);
+  const int64_t kmax = d_ff > d ? d_ff : d;
   size_t off = 0;
   L.a = off;
   off += align256((size_t)M * d * 2);
@@ -92,10 +98,11 @@ StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   off += align256((size_t)M * 3 * d * 2);
   L.u = off;
   off += align256((size_t)M * d_ff * 2);
-  L.up = off;
-  off += L.small ? 0 : align256((size_t)M * d_ff * 2);
-  L.ns = off;
-  const int64_t kmax = d_ff > d ? d_ff : d;
+  L.av = off;
+  off += L.small ? 0 : align256((size_t)M * d * 2);
+  L.ns0 = off;
+  off += L.small ? 0 : ns_bytes(M, kmax);
+  L.ns1 = off;
   off += L.small ? 0 : ns_bytes(M, kmax);
   L.total = off;
   return L;
@@ -227,8 +234,9 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
   uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
   uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + L.qkv);
   uint16_t* u = reinterpret_cast<uint16_t*>(ws + L.u);
-  uint16_t* up = reinterpret_cast<uint16_t*>(ws + L.up);
-  float* ns = reinterpret_cast<float*>(ws + L.ns);
+  uint16_t* av = reinterpret_cast<uint16_t*>(ws + L.av);
+  float* ns0 = reinterpret_cast<float*>(ws + L.ns0);
+  float* ns1 = reinterpret_cast<float*>(ws + L.ns1);
   const int64_t Mp = padded_rows(M);
   const bool small = L.small;
   hipError_t e = hipSuccess;
@@ -261,21 +269,23 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
       QL_TRY(launch_gemv(u, d_ff, Ly.down.qweight, Ly.down.scales, h, d, M, d, d_ff, 2, s));
       QL_TRY(mark(l, 3, 1));
     } else {
-      QL_TRY(launch_rmsnorm(h, a, ns, M, d, Mp, eps, true, s));
+      const GemmPrep vprep{av, d, ns1, 2 * d};   // V slice -> out-projection operand
+      const GemmPrep uprep{u, d_ff, ns1, 0};     // GELU output -> down-projection operand
+      QL_TRY(launch_rmsnorm(h, a, ns0, M, d, Mp, eps, true, s));
       QL_TRY(mark(l, 0, 0));
-      QL_TRY(launch_gemm(a, ns, Mp, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s));
+      QL_TRY(launch_gemm(a, ns0, Mp, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s,
+                         &vprep));
       QL_TRY(mark(l, 0, 1));
-      QL_TRY(launch_prep(qkv + 2 * d, 3 * d, a, ns, M, d, Mp, s));
       QL_TRY(mark(l, 1, 0));
-      QL_TRY(launch_gemm(a, ns, Mp, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
+      QL_TRY(launch_gemm(av, ns1, Mp, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
       QL_TRY(mark(l, 1, 1));
-      QL_TRY(launch_rmsnorm(h, a, ns, M, d, Mp, eps, true, s));
+      QL_TRY(launch_rmsnorm(h, a, ns0, M, d, Mp, eps, true, s));
       QL_TRY(mark(l, 2, 0));
-      QL_TRY(launch_gemm(a, ns, Mp, Ly.up.qweight, Ly.up.scales, u, d_ff, M, d_ff, d, 1, s));
+      QL_TRY(launch_gemm(a, ns0, Mp, Ly.up.qweight, Ly.up.scales, nullptr, d_ff, M, d_ff, d, 1, s,
+                         &uprep));
       QL_TRY(mark(l, 2, 1));
-      QL_TRY(launch_prep(u, d_ff, up, ns, M, d_ff, Mp, s));
       QL_TRY(mark(l, 3, 0));
-      QL_TRY(launch_gemm(up, ns, Mp, Ly.down.qweight, Ly.down.scales, h, d, M, d, d_ff, 2, s));
+      QL_TRY(launch_gemm(u, ns1, Mp, Ly.down.qweight, Ly.down.scales, h, d, M, d, d_ff, 2, s));
       QL_TRY(mark(l, 3, 1));
     }
   }

@@ -52,11 +52,26 @@ struct GemmParams {
   const float* ns;
   const uint8_t* qw;
   const uint16_t* sc;
-  void* out;
+  void* out;  // may be null when only the prepared copy is wanted
   int64_t ldo, Mp;
   int M, N, K, G;
   int tiles_m, tiles_n;
+  // prepared copy of output columns >= pcol0 (see GemmPrep)
+  uint16_t* pout;
+  float* pns;
+  int64_t pld;
+  int pcol0;
 };
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+
+// position of element e of an 8-element chunk in the MFMA operand order
+// (x0,x4,x1,x5,x2,x6,x3,x7)
+__device__ __forceinline__ int perm8(int e) { return 2 * (e & 3) + (e >> 2); }
 
 // LDS slot swizzles.  gfx950 serves a 16-byte-per-lane LDS read in four
 // cycles; one cycle takes the 4-lane quads of a half-wave whose quad index
@@ -133,29 +148,73 @@ __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets& 
   for (int j = 0; j < B_PER_WAVE; ++j) copy_to_lds<16>(qb + o.b[j], st.B + (j * NW + wave) * 64);
 }
 
-template <int EPI>
+// Epilogue.  EPI 0: bf16 store, 1: GELU then bf16, 2: fp32 residual add.
+// With PREP (EPI 0 or 1) the bf16 values of columns >= pcol0 are also written
+// as the next projection's operand: k-permuted in 8-element chunks, plus the
+// correction ns[g][m] = -136 * (sum of the group's 128 bf16 values of row m),
+// whose per-wave row sums meet in LDS (part) and are added in a fixed order.
+template <int EPI, bool PREP>
 __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, const f32x4 (&acc)[8][JF]) {
+                                           int lane, const f32x4 (&acc)[8][JF], float* part) {
   const int h = lane >> 4, lr = lane & 15;
+  float rs[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) rs[i][r] = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
 #pragma unroll
     for (int j = 0; j < JF; ++j) {
       const int64_t col = n0 + wave * WN + j * 16 + lr;
-      if (col >= p.N) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t row = m0 + i * 16 + h * 4 + r;
-        if (row >= p.M) continue;
+        const bool in = col < p.N && row < p.M;
         const float v = acc[i][j][r];
         if constexpr (EPI == 2) {
-          float* o = reinterpret_cast<float*>(p.out) + row * p.ldo + col;
-          *o = *o + v;
-        } else if constexpr (EPI == 1) {
-          reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = f32_to_bf16(gelu_erf(v));
+          if (in) {
+            float* o = reinterpret_cast<float*>(p.out) + row * p.ldo + col;
+            *o = *o + v;
+          }
         } else {
-          reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = f32_to_bf16(v);
+          const uint16_t b = f32_to_bf16(EPI == 1 ? gelu_erf(v) : v);
+          if (in && p.out) reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = b;
+          if constexpr (PREP) {
+            const int64_t c = col - p.pcol0;
+            if (in && c >= 0) p.pout[row * p.pld + (c & ~7) + perm8((int)(c & 7))] = b;
+            rs[i][r] += __uint_as_float((uint32_t)b << 16);
+          }
         }
+      }
+    }
+  }
+  if constexpr (PREP) {
+    static_assert(EPI != 2, "prepared copy of a residual update");
+    // this wave's 32 columns lie in one 128-column group of the tile
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // sum over the 16 lanes of a DPP row: quad swaps, then rotations by 4
+        // and 8 within the row
+        float t = rs[i][r];
+        t += dpp_f32<0xB1>(t);    // quad_perm [1,0,3,2]
+        t += dpp_f32<0x4E>(t);    // quad_perm [2,3,0,1]
+        t += dpp_f32<0x124>(t);   // row_ror:4
+        t += dpp_f32<0x128>(t);   // row_ror:8
+        if (lr == 0) part[wave * BM + i * 16 + h * 4 + r] = t;
+      }
+    __syncthreads();
+    // thread t: group t / 128 of the tile, row t % 128
+    const int t = threadIdx.x;
+    if (t < 2 * BM) {
+      const int gg = t / BM, m = t % BM, w0 = gg * (NW / 2);
+      const int64_t c = n0 + gg * kGroup - p.pcol0;
+      if (c >= 0 && n0 + gg * kGroup < p.N) {
+        const float sum = (part[(w0 + 0) * BM + m] + part[(w0 + 1) * BM + m]) +
+                          (part[(w0 + 2) * BM + m] + part[(w0 + 3) * BM + m]);
+        p.pns[(c / kGroup) * p.Mp + m0 + m] = -136.0f * sum;
       }
     }
   }
@@ -233,7 +292,7 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
   }
 }
 
-template <int EPI>
+template <int EPI, bool PREP>
 __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   __shared__ u32x4 sA0[A_SLOTS], sA1[A_SLOTS], sA2[A_SLOTS];
   __shared__ u32x4 sB0[B_SLOTS], sB1[B_SLOTS], sB2[B_SLOTS];
@@ -327,13 +386,18 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
 #pragma unroll
   for (int j = 0; j < JF; ++j) acc[7][j] += cprev[j] * sprev[j];
 
-  store_tile<EPI>(p, m0, n0, wave, lane, acc);
+  if constexpr (PREP) {
+    __shared__ float part[NW * BM];
+    store_tile<EPI, true>(p, m0, n0, wave, lane, acc, part);
+  } else {
+    store_tile<EPI, false>(p, m0, n0, wave, lane, acc, nullptr);
+  }
 }
 
-template <int EPI>
+template <int EPI, bool PREP>
 hipError_t launch_one(const GemmParams& p, hipStream_t s) {
   const dim3 grid((unsigned)(p.tiles_m * p.tiles_n));
-  hipLaunchKernelGGL(k_gemm<EPI>, grid, dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((k_gemm<EPI, PREP>), grid, dim3(NW * 64), 0, s, p);
   return hipGetLastError();
 }
 
@@ -343,7 +407,7 @@ hipError_t launch_one(const GemmParams& p, hipStream_t s) {
 // split here into row / column chunks that each stay below 2^31 bytes.
 hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
-                       int64_t K, int epilogue, hipStream_t s) {
+                       int64_t K, int epilogue, hipStream_t s, const GemmPrep* prep) {
   const int64_t lim = (int64_t)1 << 31;
   const int64_t mrows = std::max<int64_t>(BM, (lim / (K * 2)) / BM * BM);
   const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
@@ -355,7 +419,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
       p.ns = ns + m_s;
       p.qw = qw + n_s * (K / 2);
       p.sc = sc + n_s * (K / kGroup);
-      p.out = static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize;
+      p.out = out ? static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize : nullptr;
       p.ldo = ldo;
       p.Mp = Mp;
       p.M = (int)std::min(mrows, M - m_s);
@@ -364,11 +428,23 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
       p.G = (int)(K / kGroup);
       p.tiles_m = (p.M + BM - 1) / BM;
       p.tiles_n = (p.N + BN - 1) / BN;
+      p.pout = prep ? prep->out + m_s * prep->ld : nullptr;
+      p.pns = prep ? prep->ns + m_s : nullptr;
+      p.pld = prep ? prep->ld : 0;
+      p.pcol0 = prep ? (int)(prep->col0 - n_s) : 0;
       hipError_t e;
-      switch (epilogue) {
-        case 1: e = launch_one<1>(p, s); break;
-        case 2: e = launch_one<2>(p, s); break;
-        default: e = launch_one<0>(p, s); break;
+      if (prep) {
+        switch (epilogue) {
+          case 1: e = launch_one<1, true>(p, s); break;
+          case 2: return hipErrorInvalidValue;
+          default: e = launch_one<0, true>(p, s); break;
+        }
+      } else {
+        switch (epilogue) {
+          case 1: e = launch_one<1, false>(p, s); break;
+          case 2: e = launch_one<2, false>(p, s); break;
+          default: e = launch_one<0, false>(p, s); break;
+        }
       }
       if (e != hipSuccess) return e;
     }

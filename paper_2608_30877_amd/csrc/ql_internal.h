@@ -42,10 +42,23 @@ hipError_t launch_prep(const uint16_t* x, int64_t ldx, uint16_t* xp, float* ns, 
 hipError_t launch_rmsnorm(const float* h, uint16_t* a, float* ns, int64_t M, int64_t d,
                           int64_t Mp, float eps, bool permuted, hipStream_t s);
 
-// Large-M MFMA kernel on prepared operands.
+// Prepared copy of a projection's output (epilogue 0 or 1): the bf16 values
+// of columns col0 .. N-1 (col0 and N - col0 multiples of 128) are also
+// written as the next projection's MFMA operand, i.e. what launch_prep would
+// make of them: out [M][ld] k-permuted, ns [(N - col0)/128][Mp].
+struct GemmPrep {
+  uint16_t* out;
+  int64_t ld;
+  float* ns;
+  int64_t col0;
+};
+
+// Large-M MFMA kernel on prepared operands.  `out` may be null when `prep`
+// is given.
 hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
-                       int64_t K, int epilogue, hipStream_t s);
+                       int64_t K, int epilogue, hipStream_t s,
+                       const GemmPrep* prep = nullptr);
 
 // Small-M kernel on raw bf16 activations (M <= kSmallM).  It keeps the
 // workgroup's scales in LDS: gemv_lds_bytes(K) must stay within kGemvMaxLds

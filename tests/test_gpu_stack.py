@@ -80,6 +80,11 @@ def test_small_stack_intermediates(ql, M):
     qoff, uoff = ql.stack_workspace_offsets(M, d, dff)
     qkv = host_u16(ws[qoff:qoff + M * 3 * d * 2].view(torch.int16)).reshape(M, 3 * d)
     u = host_u16(ws[uoff:uoff + M * dff * 2].view(torch.int16)).reshape(M, dff)
+    if M > 16:
+        # the MFMA path keeps u in its operand layout: element e of every
+        # 8-element chunk sits at position 2 * (e % 4) + e // 4
+        c = np.arange(dff)
+        u = u[:, (c & ~7) + 2 * (c & 3) + ((c & 7) >> 2)]
     assert O.rel_fro(bf16_as_f64(qkv), bf16_as_f64(mid["qkv"])) <= 5e-3
     assert O.rel_fro(bf16_as_f64(u), bf16_as_f64(mid["u"])) <= 5e-3
 
