@@ -31,21 +31,30 @@ namespace {
 constexpr int NW = 8;                  // waves per workgroup
 constexpr int WN = 32;                 // columns per wave
 constexpr int JF = WN / 16;            // 16-column fragments per wave
-constexpr int BM = kGemmBM;            // 128
 constexpr int BN = NW * WN;            // 256
-constexpr int A_SLOTS = BM * 16;       // 16-byte slots per stage (32 KB)
-constexpr int B_SLOTS = BN * 4;        // 16 KB
-constexpr int A_PER_WAVE = A_SLOTS / 64 / NW;   // 4 direct-to-LDS loads per wave
-constexpr int B_PER_WAVE = B_SLOTS / 64 / NW;   // 2
+constexpr int B_SLOTS = BN * 4;        // 16-byte slots of codes per stage (16 KB)
+constexpr int B_PER_WAVE = B_SLOTS / 64 / NW;   // 2 direct-to-LDS loads per wave
 static_assert(BN == kGemmBN, "tile width");
-// Copies each wave issues per group after its single correction / scale copy
-// (see issue_stage); waiting until at most this many are outstanding means
-// every copy of the group before has landed.
-constexpr int kLaterCopies = A_PER_WAVE + B_PER_WAVE;
-static_assert(kLaterCopies < 16, "vmcnt immediate");
-// s_waitcnt immediate (gfx9 layout): vmcnt(kLaterCopies), lgkmcnt(0), expcnt
-// not waited on
-constexpr int kWaitPrevGroup = 0x0070 | kLaterCopies;
+
+// Row extent of a workgroup tile: IF 16-row fragments per wave.  128 rows
+// for large M; 64 or 32 for M <= 64, where taller tiles would spend most of
+// their MFMA work on padding rows.
+template <int IF>
+struct TileM {
+  static constexpr int BM = 16 * IF;
+  static_assert(kGemmBM % BM == 0, "correction rows are padded to kGemmBM");
+  static constexpr int A_SLOTS = BM * 16;             // 16-byte slots per stage
+  static constexpr int A_PER_WAVE = A_SLOTS / 64 / NW;
+  static constexpr int N_SLOTS = BM < 64 ? 64 : BM;   // correction terms (+ clamped copies)
+  // Copies each wave issues per group after its single correction / scale
+  // copy (see issue_stage); waiting until at most this many are outstanding
+  // means every copy of the group before has landed.
+  static constexpr int kLaterCopies = A_PER_WAVE + B_PER_WAVE;
+  static_assert(kLaterCopies < 16, "vmcnt immediate");
+  // s_waitcnt immediate (gfx9 layout): vmcnt(kLaterCopies), lgkmcnt(0),
+  // expcnt not waited on
+  static constexpr int kWaitPrevGroup = 0x0070 | kLaterCopies;
+};
 
 struct GemmParams {
   const uint16_t* xp;
@@ -126,24 +135,28 @@ struct Stage {
   uint32_t* S;  // BN scales, one zero-extended binary16 per dword
 };
 
+template <int IF>
 struct Offsets {
-  uint32_t a[A_PER_WAVE];  // byte offsets into xp of this lane's A slots (group 0)
-  uint32_t b[B_PER_WAVE];  // byte offsets into qw of this lane's B slots (group 0)
+  uint32_t a[TileM<IF>::A_PER_WAVE];  // byte offsets into xp of this lane's A slots (group 0)
+  uint32_t b[B_PER_WAVE];             // byte offsets into qw of this lane's B slots (group 0)
 };
 
-// Copies of group g into stage st.  Waves 0-1 copy the 128 correction terms,
-// waves 2-5 the 256 scales, each first; then every wave issues kLaterCopies
-// activation / code copies.
-__device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets& o, uint32_t os,
+// Copies of group g into stage st.  Waves 0-1 copy the BM correction terms
+// (rows past BM repeat the last one), waves 2-5 the 256 scales, each first;
+// then every wave issues kLaterCopies activation / code copies.
+template <int IF>
+__device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
                                             int64_t m0, int g, const Stage& st, int wave, int lane) {
+  constexpr int BM = TileM<IF>::BM;
   const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
   const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
-  if (wave < 2)
-    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + wave * 64 + lane, st.N + wave * 64);
-  else if (wave < 6)
+  if (wave * 64 < BM)
+    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + min(wave * 64 + lane, BM - 1), st.N + wave * 64);
+  else if (wave >= 2 && wave < 6)
     copy_to_lds<2>(p.sc + os + g, st.S + (wave - 2) * 64);
 #pragma unroll
-  for (int j = 0; j < A_PER_WAVE; ++j) copy_to_lds<16>(xa + o.a[j], st.A + (j * NW + wave) * 64);
+  for (int j = 0; j < TileM<IF>::A_PER_WAVE; ++j)
+    copy_to_lds<16>(xa + o.a[j], st.A + (j * NW + wave) * 64);
 #pragma unroll
   for (int j = 0; j < B_PER_WAVE; ++j) copy_to_lds<16>(qb + o.b[j], st.B + (j * NW + wave) * 64);
 }
@@ -153,17 +166,18 @@ __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets& 
 // as the next projection's operand: k-permuted in 8-element chunks, plus the
 // correction ns[g][m] = -136 * (sum of the group's 128 bf16 values of row m),
 // whose per-wave row sums meet in LDS (part) and are added in a fixed order.
-template <int EPI, bool PREP>
+template <int EPI, bool PREP, int IF>
 __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, const f32x4 (&acc)[8][JF], float* part) {
+                                           int lane, const f32x4 (&acc)[IF][JF], float* part) {
+  constexpr int BM = TileM<IF>::BM;
   const int h = lane >> 4, lr = lane & 15;
-  float rs[8][4];
+  float rs[IF][4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < IF; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) rs[i][r] = 0.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < IF; ++i) {
 #pragma unroll
     for (int j = 0; j < JF; ++j) {
       const int64_t col = n0 + wave * WN + j * 16 + lr;
@@ -193,7 +207,7 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
     static_assert(EPI != 2, "prepared copy of a residual update");
     // this wave's 32 columns lie in one 128-column group of the tile
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < IF; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         // sum over the 16 lanes of a DPP row: quad swaps, then rotations by 4
@@ -248,10 +262,11 @@ __device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
 // last fragment every read of `cur` is complete, so the wave waits for its
 // copies of the next group and joins the step barrier; the next group's
 // codes and fragment 0 are then read from `nxt` under fragment 7's MFMAs.
+template <int IF>
 __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt, int wave,
                                               int lane, bf16x8 (&bq)[JF][4], bf16x8 (&a)[4],
                                               f32x4& n4, f32x4 (&cprev)[JF], float (&sprev)[JF],
-                                              f32x4 (&acc)[8][JF]) {
+                                              f32x4 (&acc)[IF][JF]) {
   const int h = lane >> 4, lr = lane & 15;
   float scf[JF];
 #pragma unroll
@@ -259,11 +274,11 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
   bf16x8 an[4];
   f32x4 nn;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if (i + 1 < 8) {
+  for (int i = 0; i < IF; ++i) {
+    if (i + 1 < IF) {
       load_a(cur, i + 1, h, lr, an, nn);
     } else {
-      __builtin_amdgcn_s_waitcnt(kWaitPrevGroup);
+      __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
       wg_barrier();
       load_a(nxt, 0, h, lr, an, nn);
     }
@@ -276,8 +291,8 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
       for (int j = 0; j < JF; ++j) c[j] = mfma16x16x32(a[s], bq[j][s], c[j]);
     }
 #pragma unroll
-    for (int j = 0; j < JF; ++j) acc[(i + 7) & 7][j] += cprev[j] * sprev[j];
-    if (i == 7) load_b(nxt, wave, h, lr, bq);
+    for (int j = 0; j < JF; ++j) acc[(i + IF - 1) % IF][j] += cprev[j] * sprev[j];
+    if (i == IF - 1) load_b(nxt, wave, h, lr, bq);
 #pragma unroll
     for (int j = 0; j < JF; ++j) {
       cprev[j] = c[j];
@@ -292,11 +307,13 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
   }
 }
 
-template <int EPI, bool PREP>
+template <int EPI, bool PREP, int IF>
 __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
-  __shared__ u32x4 sA0[A_SLOTS], sA1[A_SLOTS], sA2[A_SLOTS];
+  using TM = TileM<IF>;
+  constexpr int BM = TM::BM;
+  __shared__ u32x4 sA0[TM::A_SLOTS], sA1[TM::A_SLOTS], sA2[TM::A_SLOTS];
   __shared__ u32x4 sB0[B_SLOTS], sB1[B_SLOTS], sB2[B_SLOTS];
-  __shared__ float sN0[BM], sN1[BM], sN2[BM];
+  __shared__ float sN0[TM::N_SLOTS], sN1[TM::N_SLOTS], sN2[TM::N_SLOTS];
   __shared__ uint32_t sS0[BN], sS1[BN], sS2[BN];
   const Stage S0{sA0, sB0, sN0, sS0}, S1{sA1, sB1, sN1, sS1}, S2{sA2, sB2, sN2, sS2};
 
@@ -322,9 +339,9 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   // per-lane source offsets of the direct-to-LDS copies (rows and columns
   // past the matrix edge are clamped: they load valid memory and their
   // results are never stored)
-  Offsets o;
+  Offsets<IF> o;
 #pragma unroll
-  for (int j = 0; j < A_PER_WAVE; ++j) {
+  for (int j = 0; j < TM::A_PER_WAVE; ++j) {
     const int slot = (j * NW + wave) * 64 + lane;
     const int row = slot >> 4;
     const int chunk = (slot & 15) ^ a_msk(row);
@@ -343,9 +360,9 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   const uint32_t os =
       (uint32_t)(min<int64_t>(n0 + ((wave - 2) & 3) * 64 + lane, p.N - 1) * p.G);
 
-  f32x4 acc[8][JF];
+  f32x4 acc[IF][JF];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < IF; ++i)
 #pragma unroll
     for (int j = 0; j < JF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -355,7 +372,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   const int G = p.G, Gl = p.G - 1;
   issue_stage(p, o, os, m0, 0, S0, wave, lane);
   issue_stage(p, o, os, m0, min(1, Gl), S1, wave, lane);
-  __builtin_amdgcn_s_waitcnt(kWaitPrevGroup);
+  __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   wg_barrier();
 
   bf16x8 bq[JF][4], a[4];
@@ -372,33 +389,42 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   int g = 0;
   for (;;) {
     issue_stage(p, o, os, m0, min(g + 2, Gl), S2, wave, lane);
-    compute_stage(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_stage<IF>(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
     issue_stage(p, o, os, m0, min(g + 2, Gl), S0, wave, lane);
-    compute_stage(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_stage<IF>(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
     issue_stage(p, o, os, m0, min(g + 2, Gl), S1, wave, lane);
-    compute_stage(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_stage<IF>(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
   }
   // no copy may still be writing LDS when the workgroup retires
   __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
-  for (int j = 0; j < JF; ++j) acc[7][j] += cprev[j] * sprev[j];
+  for (int j = 0; j < JF; ++j) acc[IF - 1][j] += cprev[j] * sprev[j];
 
   if constexpr (PREP) {
     __shared__ float part[NW * BM];
-    store_tile<EPI, true>(p, m0, n0, wave, lane, acc, part);
+    store_tile<EPI, true, IF>(p, m0, n0, wave, lane, acc, part);
   } else {
-    store_tile<EPI, false>(p, m0, n0, wave, lane, acc, nullptr);
+    store_tile<EPI, false, IF>(p, m0, n0, wave, lane, acc, nullptr);
   }
 }
 
-template <int EPI, bool PREP>
-hipError_t launch_one(const GemmParams& p, hipStream_t s) {
+template <int EPI, bool PREP, int IF>
+hipError_t launch_if(GemmParams p, hipStream_t s) {
+  p.tiles_m = (p.M + TileM<IF>::BM - 1) / TileM<IF>::BM;
   const dim3 grid((unsigned)(p.tiles_m * p.tiles_n));
-  hipLaunchKernelGGL((k_gemm<EPI, PREP>), grid, dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((k_gemm<EPI, PREP, IF>), grid, dim3(NW * 64), 0, s, p);
   return hipGetLastError();
+}
+
+// row extent by the whole call's M (every chunk of a split call uses one)
+template <int EPI, bool PREP>
+hipError_t launch_one(const GemmParams& p, int64_t M, hipStream_t s) {
+  if (M <= 32) return launch_if<EPI, PREP, 2>(p, s);
+  if (M <= 64) return launch_if<EPI, PREP, 4>(p, s);
+  return launch_if<EPI, PREP, 8>(p, s);
 }
 
 }  // namespace
@@ -409,7 +435,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
                        int64_t K, int epilogue, hipStream_t s, const GemmPrep* prep) {
   const int64_t lim = (int64_t)1 << 31;
-  const int64_t mrows = std::max<int64_t>(BM, (lim / (K * 2)) / BM * BM);
+  const int64_t mrows = std::max<int64_t>(kGemmBM, (lim / (K * 2)) / kGemmBM * kGemmBM);
   const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
   const size_t esize = epilogue == 2 ? 4 : 2;
   for (int64_t m_s = 0; m_s < M; m_s += mrows) {
@@ -426,7 +452,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
       p.N = (int)std::min(ncols, N - n_s);
       p.K = (int)K;
       p.G = (int)(K / kGroup);
-      p.tiles_m = (p.M + BM - 1) / BM;
+      p.tiles_m = 0;  // set per row extent in launch_if
       p.tiles_n = (p.N + BN - 1) / BN;
       p.pout = prep ? prep->out + m_s * prep->ld : nullptr;
       p.pns = prep ? prep->ns + m_s : nullptr;
@@ -435,15 +461,15 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
       hipError_t e;
       if (prep) {
         switch (epilogue) {
-          case 1: e = launch_one<1, true>(p, s); break;
+          case 1: e = launch_one<1, true>(p, M, s); break;
           case 2: return hipErrorInvalidValue;
-          default: e = launch_one<0, true>(p, s); break;
+          default: e = launch_one<0, true>(p, M, s); break;
         }
       } else {
         switch (epilogue) {
-          case 1: e = launch_one<1, false>(p, s); break;
-          case 2: e = launch_one<2, false>(p, s); break;
-          default: e = launch_one<0, false>(p, s); break;
+          case 1: e = launch_one<1, false>(p, M, s); break;
+          case 2: e = launch_one<2, false>(p, M, s); break;
+          default: e = launch_one<0, false>(p, M, s); break;
         }
       }
       if (e != hipSuccess) return e;

@@ -101,9 +101,10 @@ def test_dequant_bit_exact(ql, N, K):
 
 # ------------------------------------------------------------------ forward
 
-SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel, ragged tails
+SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel (32-, 64- and 128-row tiles), ragged tails
     (1, 64, 128), (5, 250, 384), (8, 512, 512), (16, 512, 512), (16, 1000, 1280),
-    (17, 256, 256), (64, 384, 512), (128, 256, 512), (200, 500, 640), (300, 1024, 1152),
+    (17, 256, 256), (32, 256, 384), (48, 300, 256), (64, 384, 512), (128, 256, 512),
+    (200, 500, 640), (300, 1024, 1152),
     # the largest K whose scales the small-batch kernel keeps in LDS, and the
     # next group up, which a small batch runs on the MFMA kernel instead
     (3, 70, 49152), (8, 96, 49280),

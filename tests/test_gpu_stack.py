@@ -52,9 +52,10 @@ def _run(ql, dev_layers, h0, dff, n_layers=None):
     return h, ws
 
 
-@pytest.mark.parametrize("M", [8, 16, 64, 200])
+@pytest.mark.parametrize("M", [8, 16, 24, 64, 200])
 def test_small_stack_end_to_end(ql, M):
-    """4 blocks at d = 256, d_ff = 1024 (both kernels: M <= 16 and M > 16)."""
+    """4 blocks at d = 256, d_ff = 1024 (small-batch kernel for M <= 16, MFMA
+    kernel with 32-, 64- and 128-row tiles above)."""
     d, dff, L = 256, 1024, 4
     say(f"stack M={M} d={d} L={L}")
     layers = [_packed_layer_oracle(40, l, d, dff) for l in range(L)]
@@ -69,7 +70,7 @@ def test_small_stack_end_to_end(ql, M):
     assert err <= 5e-3
 
 
-@pytest.mark.parametrize("M", [8, 64])
+@pytest.mark.parametrize("M", [8, 24, 64])
 def test_small_stack_intermediates(ql, M):
     """One block: the workspace's qkv and u buffers against the oracle's."""
     d, dff = 256, 1024
