@@ -115,6 +115,11 @@ hipError_t launch_prep(const uint16_t* x, int64_t ldx, uint16_t* xp, float* ns, 
 // ---------------------------------------------------------------------------
 // RMSNorm (unit gain): one workgroup per row, two passes over the row.
 // ---------------------------------------------------------------------------
+// One row per 256-thread block: thread t owns chunks t, t + 256, ... (8
+// elements each).  The row is held in registers between the sum of squares
+// and the scaling when it fits CPT chunks per thread (CPT = 0: re-read it).
+// The same chunk order either way, so the result does not depend on CPT.
+template <int CPT>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
                                                  uint16_t* __restrict__ a, float* __restrict__ ns,
                                                  int64_t d, int64_t Mp, float eps, int permuted) {
@@ -122,12 +127,34 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
   const int64_t m = blockIdx.x;
   const float* row = h + m * d;
   const int64_t nchunks = d / 8;
+  constexpr int R = CPT > 0 ? CPT : 1;
+  float4 P[R], Q[R];
   float ss = 0.0f;
-  for (int64_t c = threadIdx.x; c < nchunks; c += 256) {
-    const float4 p = *reinterpret_cast<const float4*>(row + c * 8);
-    const float4 q = *reinterpret_cast<const float4*>(row + c * 8 + 4);
-    ss += (p.x * p.x + p.y * p.y) + (p.z * p.z + p.w * p.w) + (q.x * q.x + q.y * q.y) +
-          (q.z * q.z + q.w * q.w);
+  if constexpr (CPT > 0) {
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int64_t c = k * 256 + threadIdx.x;
+      if (c < nchunks) {
+        P[k] = *reinterpret_cast<const float4*>(row + c * 8);
+        Q[k] = *reinterpret_cast<const float4*>(row + c * 8 + 4);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int64_t c = k * 256 + threadIdx.x;
+      if (c < nchunks) {
+        const float4 p = P[k], q = Q[k];
+        ss += (p.x * p.x + p.y * p.y) + (p.z * p.z + p.w * p.w) + (q.x * q.x + q.y * q.y) +
+              (q.z * q.z + q.w * q.w);
+      }
+    }
+  } else {
+    for (int64_t c = threadIdx.x; c < nchunks; c += 256) {
+      const float4 p = *reinterpret_cast<const float4*>(row + c * 8);
+      const float4 q = *reinterpret_cast<const float4*>(row + c * 8 + 4);
+      ss += (p.x * p.x + p.y * p.y) + (p.z * p.z + p.w * p.w) + (q.x * q.x + q.y * q.y) +
+            (q.z * q.z + q.w * q.w);
+    }
   }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -135,12 +162,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
   // chunk loop with a trip count uniform across the block (shuffles below)
-  for (int64_t c0 = 0; c0 < nchunks; c0 += 256) {
-    const int64_t c = c0 + threadIdx.x;
+  auto emit = [&](int64_t c, const float4& p, const float4& q) {
     float sum = 0.0f;
     if (c < nchunks) {
-      const float4 p = *reinterpret_cast<const float4*>(row + c * 8);
-      const float4 q = *reinterpret_cast<const float4*>(row + c * 8 + 4);
       const uint16_t b0 = f32_to_bf16(p.x * r), b1 = f32_to_bf16(p.y * r);
       const uint16_t b2 = f32_to_bf16(p.z * r), b3 = f32_to_bf16(p.w * r);
       const uint16_t b4 = f32_to_bf16(q.x * r), b5 = f32_to_bf16(q.y * r);
@@ -161,13 +185,35 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
       sum = sum16(sum);
       if ((threadIdx.x & 15) == 0 && c < nchunks) ns[(c / 16) * Mp + m] = -136.0f * sum;
     }
+  };
+  if constexpr (CPT > 0) {
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      if ((int64_t)k * 256 >= nchunks) break;   // uniform across the block
+      emit(k * 256 + threadIdx.x, P[k], Q[k]);
+    }
+  } else {
+    for (int64_t c0 = 0; c0 < nchunks; c0 += 256) {
+      const int64_t c = c0 + threadIdx.x;
+      float4 p = {0.f, 0.f, 0.f, 0.f}, q = p;
+      if (c < nchunks) {
+        p = *reinterpret_cast<const float4*>(row + c * 8);
+        q = *reinterpret_cast<const float4*>(row + c * 8 + 4);
+      }
+      emit(c, p, q);
+    }
   }
 }
 
 hipError_t launch_rmsnorm(const float* h, uint16_t* a, float* ns, int64_t M, int64_t d,
                           int64_t Mp, float eps, bool permuted, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3((unsigned)M), dim3(256), 0, s, h, a, ns, d, Mp, eps,
-                     permuted ? 1 : 0);
+  const int64_t cpt = (d / 8 + 255) / 256;   // chunks per thread
+  const dim3 grid((unsigned)M), block(256);
+  const int pm = permuted ? 1 : 0;
+  if (cpt <= 2) hipLaunchKernelGGL(k_rmsnorm<2>, grid, block, 0, s, h, a, ns, d, Mp, eps, pm);
+  else if (cpt <= 4) hipLaunchKernelGGL(k_rmsnorm<4>, grid, block, 0, s, h, a, ns, d, Mp, eps, pm);
+  else if (cpt <= 8) hipLaunchKernelGGL(k_rmsnorm<8>, grid, block, 0, s, h, a, ns, d, Mp, eps, pm);
+  else hipLaunchKernelGGL(k_rmsnorm<0>, grid, block, 0, s, h, a, ns, d, Mp, eps, pm);
   return hipGetLastError();
 }
 

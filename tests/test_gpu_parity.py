@@ -356,7 +356,7 @@ def test_max_size_launch_split_bit_exact(ql, M, N, K):
 
 # ------------------------------------------------------------------ RMSNorm
 
-@pytest.mark.parametrize("M,d", [(3, 256), (64, 12288)])
+@pytest.mark.parametrize("M,d", [(3, 256), (64, 12288), (2, 20480)])
 def test_rmsnorm(ql, M, d):
     h = synth.residual_f32(M + d, M, d) * np.float32(3.0)
     a = host_u16(ql.rmsnorm(dev(h)))
