@@ -95,30 +95,73 @@ __device__ __forceinline__ int a_msk(int row) {
 __device__ __forceinline__ int a_phys(int row, int chunk) { return chunk ^ a_msk(row); }
 __device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2)) & 3; }
 
-// Direct-to-LDS copy of BYTES per lane: lane l writes lds + l * BYTES (a
-// 2-byte copy writes its value zero-extended into the dword lds + 4 * l).
-// Written as inline assembly so that the compiler does not track these loads:
-// its own wait insertion cannot tell the three ring stages apart and would
-// wait for the copies just issued before every LDS read.  The kernel waits
-// for them explicitly (kWaitPrevGroup before the step barrier, vmcnt(0)
-// before the epilogue), and issues no other vector memory load in its loop.
-// M0 carries the LDS base; one wait state must separate its write from the
-// load that reads it.
+// Direct-to-LDS copies: lane l writes lds + l * BYTES (a 2-byte copy writes
+// its value zero-extended into the dword lds + 4 * l).  Written as inline
+// assembly so that the compiler does not track these loads: its own wait
+// insertion cannot tell the three ring stages apart and would wait for the
+// copies just issued before every LDS read.  The kernel waits for them
+// explicitly (kWaitPrevGroup before the step barrier, vmcnt(0) before the
+// epilogue), and issues no other vector memory load in its loop.  M0 carries
+// the LDS base (one wait state must separate its write from the load that
+// reads it); M0 is a register the compiler reserves, so each sequence saves
+// and restores it instead of clobbering it.
+#define QL_LDS_COPY(OP, A, L) "s_mov_b32 m0, %[" L "]\n\ts_nop 0\n\t" OP " %[" A "], off\n\t"
+
+// one 2- or 4-byte copy (correction terms, scales)
 template <int BYTES>
 __device__ __forceinline__ void copy_to_lds(const void* src, const void* lds) {
   const uint32_t l = (uint32_t)reinterpret_cast<uintptr_t>(lds);
-  if constexpr (BYTES == 16) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :: "v"(src), "s"(l) : "memory", "m0");
-  } else if constexpr (BYTES == 4) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
-                 :: "v"(src), "s"(l) : "memory", "m0");
+  uint32_t saved;
+  if constexpr (BYTES == 4) {
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dword", "a", "l")
+                 "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved) : [a] "v"(src), [l] "s"(l) : "memory");
   } else {
     static_assert(BYTES == 2, "copy width");
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_ushort %0, off"
-                 :: "v"(src), "s"(l) : "memory", "m0");
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_ushort", "a", "l")
+                 "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved) : [a] "v"(src), [l] "s"(l) : "memory");
   }
 }
+
+// NA 16-byte activation copies then two 16-byte code copies, in one sequence
+template <int NA>
+__device__ __forceinline__ void copy16_to_lds(const void* const (&a)[NA], const uint32_t (&la)[NA],
+                                              const void* b0, uint32_t lb0, const void* b1,
+                                              uint32_t lb1) {
+  uint32_t saved;
+#define QL_X16 "global_load_lds_dwordx4"
+  if constexpr (NA == 1) {
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
+                 QL_LDS_COPY(QL_X16, "b0", "m0v") QL_LDS_COPY(QL_X16, "b1", "m1v")
+                 "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved)
+                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1),
+                   [m1v] "s"(lb1)
+                 : "memory");
+  } else if constexpr (NA == 2) {
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
+                 QL_LDS_COPY(QL_X16, "a1", "l1") QL_LDS_COPY(QL_X16, "b0", "m0v")
+                 QL_LDS_COPY(QL_X16, "b1", "m1v") "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved)
+                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [a1] "v"(a[1]), [l1] "s"(la[1]),
+                   [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1), [m1v] "s"(lb1)
+                 : "memory");
+  } else {
+    static_assert(NA == 4, "activation copies per wave");
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
+                 QL_LDS_COPY(QL_X16, "a1", "l1") QL_LDS_COPY(QL_X16, "a2", "l2")
+                 QL_LDS_COPY(QL_X16, "a3", "l3") QL_LDS_COPY(QL_X16, "b0", "m0v")
+                 QL_LDS_COPY(QL_X16, "b1", "m1v") "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved)
+                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [a1] "v"(a[1]), [l1] "s"(la[1]),
+                   [a2] "v"(a[2]), [l2] "s"(la[2]), [a3] "v"(a[3]), [l3] "s"(la[3]),
+                   [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1), [m1v] "s"(lb1)
+                 : "memory");
+  }
+#undef QL_X16
+}
+#undef QL_LDS_COPY
 
 // Workgroup barrier without the memory fence of __syncthreads (which would
 // also wait for every copy in flight).
@@ -154,11 +197,18 @@ __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<I
     copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + min(wave * 64 + lane, BM - 1), st.N + wave * 64);
   else if (wave >= 2 && wave < 6)
     copy_to_lds<2>(p.sc + os + g, st.S + (wave - 2) * 64);
+  constexpr int NA = TileM<IF>::A_PER_WAVE;
+  static_assert(B_PER_WAVE == 2, "two code copies per wave");
+  const void* asrc[NA];
+  uint32_t alds[NA];
 #pragma unroll
-  for (int j = 0; j < TileM<IF>::A_PER_WAVE; ++j)
-    copy_to_lds<16>(xa + o.a[j], st.A + (j * NW + wave) * 64);
-#pragma unroll
-  for (int j = 0; j < B_PER_WAVE; ++j) copy_to_lds<16>(qb + o.b[j], st.B + (j * NW + wave) * 64);
+  for (int j = 0; j < NA; ++j) {
+    asrc[j] = xa + o.a[j];
+    alds[j] = (uint32_t)reinterpret_cast<uintptr_t>(st.A + (j * NW + wave) * 64);
+  }
+  copy16_to_lds<NA>(asrc, alds, qb + o.b[0],
+                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (0 * NW + wave) * 64), qb + o.b[1],
+                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (1 * NW + wave) * 64));
 }
 
 // Epilogue.  EPI 0: bf16 store, 1: GELU then bf16, 2: fp32 residual add.
