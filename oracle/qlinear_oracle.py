@@ -25,9 +25,11 @@ this library fixes it, and the functions below are that scheme written out:
   * Y = fp64(x) fp64(W_dq)^T with x the given bf16 values; stored results
     are bf16 (round to nearest even) unless the step keeps fp32.
 
-The transformer-block steps (RMSNorm, GELU, the width-1 sliding-window
-stand-in between the QKV and output projections, fp32 residual stream) are
-written out in ``rmsnorm_bf16``, ``gelu`` and ``stack_layer``.
+The transformer-block steps (RMSNorm, GELU, the attention between the QKV
+and output projections -- either the width-1 sliding-window stand-in or the
+causal sliding-window attention of ``attention_ref`` -- fp32 residual
+stream) are written out in ``rmsnorm_bf16``, ``gelu``, ``attention_ref`` and
+``stack_layer``.
 
 Every function here is pinned by CPU tests against something other than
 itself: exact rational brute force, closed forms, special cases, library
@@ -42,7 +44,7 @@ __all__ = [
     "GROUP", "QMAX", "QMIN", "ERR_RANGE", "OracleRangeError",
     "bf16_bits_to_f64", "f64_to_bf16_bits", "f16_bits_to_f32",
     "quantize_pack", "unpack_codes", "dequant", "qlinear_ref",
-    "qlinear_ref_cols", "gelu", "rmsnorm_bf16", "stack_layer",
+    "qlinear_ref_cols", "gelu", "rmsnorm_bf16", "attention_ref", "stack_layer",
     "rel_fro",
 ]
 
@@ -192,15 +194,18 @@ def rmsnorm_bf16(h: np.ndarray, eps: float = 1e-5) -> np.ndarray:
 
 
 def stack_layer(h: np.ndarray, layer: dict, group: int = GROUP, eps: float = 1e-5,
-                keep: bool = False):
+                keep: bool = False, attn=None):
     """One block of the 175B-shaped linear stack on the fp32 residual h [M, d].
 
     layer = {"qkv": (qw, s), "out": (qw, s), "up": (qw, s), "down": (qw, s)}
     with the QKV projection's output columns ordered [Q | K | V].
 
-    Steps:  a = RMSNorm(h);  qkv = bf16(a W_qkv^T);  v = qkv[:, 2d:3d]
-            (a sliding window of width 1 makes attention the identity on V,
-            the paper's model uses sliding-window attention, Sec. 1 / 2.1);
+    Steps:  a = RMSNorm(h);  qkv = bf16(a W_qkv^T);
+            v = qkv[:, 2d:3d] when attn is None (a sliding window of width 1
+            makes attention the identity on V), else
+            v = bf16(attention_ref(qkv, d, *attn)) with attn = (heads,
+            seq_len, window) (the paper's model uses sliding-window
+            attention, Sec. 1 / 2);
             h1 = fp32(h + v W_o^T);  a2 = RMSNorm(h1);
             u = bf16(GELU(a2 W_up^T));  h2 = fp32(h1 + u W_down^T).
     Returns h2 (and the intermediates when keep=True).
@@ -209,14 +214,55 @@ def stack_layer(h: np.ndarray, layer: dict, group: int = GROUP, eps: float = 1e-
     d = h.shape[1]
     a = rmsnorm_bf16(h, eps)
     qkv = f64_to_bf16_bits(qlinear_ref(a, *layer["qkv"], group=group))
-    v = np.ascontiguousarray(qkv[:, 2 * d:3 * d])
+    if attn is None:
+        v = np.ascontiguousarray(qkv[:, 2 * d:3 * d])
+    else:
+        v = f64_to_bf16_bits(attention_ref(qkv, d, *attn))
     h1 = (h.astype(np.float64) + qlinear_ref(v, *layer["out"], group=group)).astype(np.float32)
     a2 = rmsnorm_bf16(h1, eps)
     u = f64_to_bf16_bits(gelu(qlinear_ref(a2, *layer["up"], group=group)))
     h2 = (h1.astype(np.float64) + qlinear_ref(u, *layer["down"], group=group)).astype(np.float32)
     if keep:
-        return h2, {"a": a, "qkv": qkv, "h1": h1, "a2": a2, "u": u}
+        return h2, {"a": a, "qkv": qkv, "v": v, "h1": h1, "a2": a2, "u": u}
     return h2
+
+
+def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len: int,
+                  window: int) -> np.ndarray:
+    """Causal sliding-window multi-head attention of the paper's decoder
+    (sliding-window attention with a 32K window, Sec. 1 contribution 1.1 and
+    Sec. 2), fp64 from the given bf16 Q, K, V.
+
+    qkv_bits [M, 3d] bf16 bits, columns [Q | K | V]; head h uses columns
+    h*dh .. h*dh+dh-1 of each third, dh = d / heads.  The M tokens are M /
+    seq_len independent sequences (one protein-ligand pair each) of seq_len
+    tokens; token i of a sequence attends to tokens j of the same sequence
+    with i - window < j <= i.  Per head:
+        S = Q K^T / sqrt(dh),  P = softmax over the allowed keys (row-wise),
+        O = P V.
+    Returns O [M, d] (fp64), heads side by side in the column order of Q.
+    """
+    x = bf16_bits_to_f64(np.asarray(qkv_bits))
+    M = x.shape[0]
+    dh = d // heads
+    if d % heads or M % seq_len:
+        raise ValueError("d must split into heads and M into whole sequences")
+    out = np.empty((M, d), dtype=np.float64)
+    i = np.arange(seq_len)[:, None]
+    j = np.arange(seq_len)[None, :]
+    allowed = (j <= i) & (j > i - window)
+    for p0 in range(0, M, seq_len):
+        rows = slice(p0, p0 + seq_len)
+        for hh in range(heads):
+            c = slice(hh * dh, (hh + 1) * dh)
+            q = x[rows, c]
+            k = x[rows, d + hh * dh:d + (hh + 1) * dh]
+            v = x[rows, 2 * d + hh * dh:2 * d + (hh + 1) * dh]
+            s = (q @ k.T) / np.sqrt(dh)
+            s = np.where(allowed, s, -np.inf)
+            e = np.exp(s - s.max(axis=1, keepdims=True))
+            out[rows, c] = (e / e.sum(axis=1, keepdims=True)) @ v
+    return out
 
 
 def rel_fro(y: np.ndarray, ref: np.ndarray) -> float:

@@ -334,3 +334,97 @@ def test_stack_layer_v_slice_and_gelu_placement():
     g = O.bf16_bits_to_f64(O.f64_to_bf16_bits(
         0.5 * a2 * (1 + np.vectorize(math.erf)(a2 / math.sqrt(2)))))
     np.testing.assert_array_equal(h2, (h1.astype(np.float64) + g).astype(np.float32))
+
+
+# ------------------------------------------------------------------ attention
+
+def _qkv(q, k, v):
+    """bf16 bit patterns of [Q | K | V] from fp64 blocks (values are rounded
+    to bf16 first; the pins below compute their expectations from the rounded
+    values)."""
+    return O.f64_to_bf16_bits(np.concatenate([q, k, v], axis=1))
+
+
+def test_attention_zero_keys_is_causal_running_mean():
+    """K = 0: every allowed score is 0, so token i averages V over
+    max(0, i - window + 1) .. i of its own sequence (closed form)."""
+    rng = np.random.default_rng(5)
+    d, heads, L, window = 8, 2, 6, 4
+    M = 2 * L
+    q = rng.standard_normal((M, d))
+    v = rng.standard_normal((M, d))
+    bits = _qkv(q, np.zeros((M, d)), v)
+    vr = O.bf16_bits_to_f64(bits[:, 2 * d:])
+    out = O.attention_ref(bits, d, heads, L, window)
+    for p in range(2):
+        for i in range(L):
+            lo = max(0, i - window + 1)
+            ref = vr[p * L + lo:p * L + i + 1].mean(axis=0)
+            np.testing.assert_allclose(out[p * L + i], ref, rtol=0, atol=1e-14)
+
+
+def test_attention_window_one_is_identity_on_v():
+    """A window of one token reduces attention to the V slice: the width-1
+    stand-in of the linear stack."""
+    rng = np.random.default_rng(6)
+    d, M = 16, 10
+    bits = _qkv(rng.standard_normal((M, d)), rng.standard_normal((M, d)),
+                rng.standard_normal((M, d)))
+    out = O.attention_ref(bits, d, 4, 5, 1)
+    np.testing.assert_array_equal(out, O.bf16_bits_to_f64(bits[:, 2 * d:]))
+
+
+def test_attention_two_token_weights_by_hand():
+    """One head, dh = 2: token 1 sees keys 0 and 1 with scores s0 = q.k0 /
+    sqrt(2) and s1 = 0, so its output is (e^s0 V0 + V1) / (e^s0 + 1); token 0
+    sees only itself."""
+    d = 2
+    k0 = O.bf16_bits_to_f64(O.f64_to_bf16_bits(np.array([math.sqrt(2) * math.log(3.0)])))[0]
+    q = np.array([[0.0, 0.0], [1.0, 0.0]])
+    k = np.array([[k0, 0.0], [0.0, 0.0]])
+    v = np.array([[2.0, -1.0], [6.0, 3.0]])
+    out = O.attention_ref(_qkv(q, k, v), d, 1, 2, 8)
+    w0 = math.exp(k0 / math.sqrt(2))          # ~ 3
+    np.testing.assert_allclose(out[0], v[0], rtol=0, atol=0)
+    np.testing.assert_allclose(out[1], (w0 * v[0] + v[1]) / (w0 + 1.0), rtol=1e-14, atol=1e-14)
+    assert abs(w0 - 3.0) < 0.02                 # the weights are about 3/4, 1/4
+
+
+def test_attention_dominant_key_selects_its_value():
+    """A score far above the others puts (all but e^-100 of) the weight on one
+    key: the output is that key's V row."""
+    rng = np.random.default_rng(7)
+    d, heads, L = 8, 1, 5
+    q = np.zeros((L, d))
+    k = np.zeros((L, d))
+    v = rng.standard_normal((L, d))
+    q[4, 0] = 16.0
+    k[2, 0] = 16.0                              # score 256 / sqrt(8) ~ 90.5
+    bits = _qkv(q, k, v)
+    out = O.attention_ref(bits, d, heads, L, L)
+    np.testing.assert_allclose(out[4], O.bf16_bits_to_f64(bits[2, 2 * d:]), rtol=0, atol=1e-30)
+
+
+def test_attention_causal_and_sequence_local():
+    """Changing a later token of a sequence, or another sequence entirely,
+    leaves the earlier outputs of the sequence unchanged."""
+    rng = np.random.default_rng(8)
+    d, heads, L = 8, 2, 6
+    M = 2 * L
+    blocks = [rng.standard_normal((M, d)) for _ in range(3)]
+    base = O.attention_ref(_qkv(*blocks), d, heads, L, L)
+    changed = [b.copy() for b in blocks]
+    for b in changed:
+        b[4] += 3.0                             # token 4 of sequence 0
+        b[L:] = rng.standard_normal((L, d))     # all of sequence 1
+    out = O.attention_ref(_qkv(*changed), d, heads, L, L)
+    np.testing.assert_array_equal(out[:4], base[:4])
+
+
+def test_stack_layer_with_width_one_attention_matches_stand_in():
+    """stack_layer with attention of window 1 is the width-1 stand-in."""
+    d, dff, M = 128, 256, 6
+    mk = lambda i, n, k: O.quantize_pack(synth.weights_f32(50 + i, n, k))
+    layer = {"qkv": mk(0, 3 * d, d), "out": mk(1, d, d), "up": mk(2, dff, d), "down": mk(3, d, dff)}
+    h = synth.residual_f32(9, M, d)
+    np.testing.assert_array_equal(O.stack_layer(h, layer), O.stack_layer(h, layer, attn=(1, 3, 1)))
