@@ -165,7 +165,7 @@ size_t qlayer_stack_workspace_bytes(int64_t M, int64_t d, int64_t d_ff,
  *              256-byte aligned.  Layout (byte offsets, each 256-aligned):
  *              [0]        a / a2 staging  bf16 [M][d]   (internal layout)
  *              [qkv_off]  qkv             bf16 [M][3d]  (row-major)
- *              [u_off]    u               bf16 [M][d_ff]: row-major when
+ *              [u_off]    u               bf16 [M][max(d, d_ff)]: row-major when
  *                         M <= 16; for larger M the MFMA operand layout,
  *                         in which each 8-element chunk of a row holds
  *                         elements (0,4,1,5,2,6,3,7) of that chunk
@@ -191,6 +191,55 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
                                int64_t M, int64_t d, int64_t d_ff, int32_t group,
                                float eps, void* workspace, size_t ws_bytes,
                                void* const* events, ql_stream_t stream);
+
+/*
+ * qlinear_attention -- causal sliding-window multi-head attention, the
+ * attention of the paper's decoder (a 32K sliding window, Sec. 1
+ * contribution 1.1 and Sec. 2), run between the QKV and output projections.
+ * The M tokens form M / seq_len independent sequences (one protein-ligand
+ * pair each); token i of a sequence attends to the tokens j of the same
+ * sequence with i - window < j <= i.  Per head (head dim 128):
+ *     O = softmax(Q K^T / sqrt(128) restricted to the window) V
+ * Scores and softmax in fp32; the probabilities are rounded to bf16 for the
+ * product with V and the normaliser sums the rounded values; fp32
+ * accumulation; bf16 output, rounded to nearest even.
+ *   qkv     bf16 bits, row m at qkv + m*ldqkv: Q in columns 0..d-1, K in
+ *           d..2d-1, V in 2d..3d-1; head h uses columns 128h..128h+127 of
+ *           each third (the layout of the QKV projection's output).
+ *   out     bf16 bits, row m at out + m*ldo, columns 0..d-1 written (heads
+ *           side by side); must not overlap qkv (QL_ERR_ARG).
+ *   d       heads * 128 (any other head dimension: QL_ERR_UNSUPPORTED).
+ *   seq_len >= 1 with M % seq_len == 0; window >= 1 (window >= seq_len is
+ *           plain causal attention within each sequence).
+ *   ldqkv >= 3d and ldo >= d, both multiples of 8 elements, and qkv and out
+ *   16-byte aligned (QL_ERR_ALIGN otherwise).
+ */
+int qlinear_attention(const uint16_t* qkv, int64_t ldqkv, uint16_t* out,
+                      int64_t ldo, int64_t M, int64_t d, int32_t heads,
+                      int32_t seq_len, int32_t window, ql_stream_t stream);
+
+/* Attention between the QKV and output projections of a stack block. */
+typedef struct {
+    int32_t heads;    /* 0 selects the width-1 stand-in v = qkv[:, 2d:3d]   */
+    int32_t seq_len;  /* tokens per sequence (M % seq_len == 0)             */
+    int32_t window;   /* sliding-window width, >= 1                         */
+} ql_attention_cfg;
+
+/*
+ * qlayer_stack_forward_attn -- qlayer_stack_forward_timed with attention:
+ * in every block v = qlinear_attention(qkv) (bf16) replaces the stand-in
+ * v = qkv[:, 2d:3d].  attn NULL or attn->heads == 0 runs the stand-in.
+ * Requirements on heads, seq_len and window as for qlinear_attention, with
+ * d = heads * 128.  The attention output is staged in the workspace's u
+ * buffer (row-major [M][d]) before the out projection; the workspace is the
+ * same size.  With events, attention runs between events[8l + 1] and
+ * events[8l + 2].
+ */
+int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h,
+                              int64_t M, int64_t d, int64_t d_ff, int32_t group,
+                              float eps, const ql_attention_cfg* attn,
+                              void* workspace, size_t ws_bytes,
+                              void* const* events, ql_stream_t stream);
 
 /* Host: byte offsets of the qkv and u buffers inside the stack workspace. */
 void qlayer_stack_workspace_offsets(int64_t M, int64_t d, int64_t d_ff,

@@ -19,7 +19,7 @@ __all__ = [
     "LIB_PATH", "QLError", "lib", "GROUP", "EPI_NONE", "EPI_GELU", "EPI_RESID_F32",
     "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
-    "stack_forward_timed", "make_layers", "release",
+    "stack_forward_timed", "make_layers", "release", "attention",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
@@ -56,6 +56,9 @@ def _load():
         "qlayer_stack_forward_timed": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
                                                       ctypes.c_float, vp, sz, vp, vp]),
         "qlinear_rmsnorm": (ctypes.c_int, [vp, vp, i64, i64, ctypes.c_float, vp]),
+        "qlinear_attention": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, i32, i32, vp]),
+        "qlayer_stack_forward_attn": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
+                                                     ctypes.c_float, vp, vp, sz, vp, vp]),
         "qlinear_release": (None, []),
     }
     for name, (res, args) in sig.items():
@@ -101,6 +104,19 @@ def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
 
 
 _BITS16 = (torch.bfloat16, torch.int16, torch.uint16, torch.float16)
+
+
+class _AttnCfg(ctypes.Structure):
+    _fields_ = [("heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("window", ctypes.c_int32)]
+
+
+def _attn_cfg(attn):
+    """None or (heads, seq_len, window) -> pointer to a ql_attention_cfg (or None)."""
+    if attn is None:
+        return None
+    heads, seq_len, window = (int(v) for v in attn)
+    return ctypes.pointer(_AttnCfg(heads, seq_len, window))
 
 
 class _QLayer(ctypes.Structure):
@@ -191,6 +207,27 @@ def rmsnorm(h: torch.Tensor, eps: float = 1e-5, stream=None):
     return a
 
 
+def attention(qkv: torch.Tensor, heads: int, seq_len: int, window: int,
+              out: torch.Tensor | None = None, stream=None):
+    """Causal sliding-window attention over a [Q | K | V] bf16 buffer
+    qkv [M, >= 3d] (row stride qkv.stride(0)), d = 128 * heads; returns
+    out [M, d] bf16 (or writes the caller's `out`, row stride out.stride(0))."""
+    if not isinstance(qkv, torch.Tensor) or not qkv.is_cuda or qkv.dtype not in _BITS16 \
+            or qkv.dim() != 2 or qkv.stride(1) != 1:
+        raise ValueError("qkv must be a 2-D CUDA bf16 tensor with unit column stride")
+    M = qkv.shape[0]
+    d = 128 * int(heads)
+    if out is None:
+        out = torch.empty((M, d), dtype=torch.bfloat16, device=qkv.device)
+    if not isinstance(out, torch.Tensor) or not out.is_cuda or out.dtype not in _BITS16 \
+            or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be a 2-D CUDA bf16 tensor with unit column stride")
+    _check(lib.qlinear_attention(_ptr(qkv), qkv.stride(0), _ptr(out), out.stride(0), M, d,
+                                 int(heads), int(seq_len), int(window), _stream(stream)),
+           "qlinear_attention")
+    return out
+
+
 def stack_workspace_bytes(M: int, d: int, d_ff: int, group: int = GROUP) -> int:
     return int(lib.qlayer_stack_workspace_bytes(M, d, d_ff, group))
 
@@ -215,21 +252,29 @@ def make_layers(layers):
 
 def stack_forward(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tensor,
                   n_layers: int | None = None, eps: float = 1e-5, group: int = GROUP,
-                  stream=None):
-    """Run the linear stack in place on the fp32 residual h [M, d]."""
+                  stream=None, attn=None):
+    """Run the linear stack in place on the fp32 residual h [M, d].  attn =
+    (heads, seq_len, window) runs sliding-window attention between the QKV
+    and out projections; None runs the width-1 stand-in."""
     _need(h, "h", (torch.float32,), 2)
     M, d = h.shape
     n = len(layers_arr) if n_layers is None else n_layers
     ws_n = workspace.numel() * workspace.element_size()
-    _check(lib.qlayer_stack_forward(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h), M, d,
-                                    d_ff, group, eps, _ptr(workspace), ws_n, _stream(stream)),
-           "qlayer_stack_forward")
+    if attn is None:
+        rc = lib.qlayer_stack_forward(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h), M, d,
+                                      d_ff, group, eps, _ptr(workspace), ws_n, _stream(stream))
+        _check(rc, "qlayer_stack_forward")
+    else:
+        rc = lib.qlayer_stack_forward_attn(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
+                                           M, d, d_ff, group, eps, _attn_cfg(attn),
+                                           _ptr(workspace), ws_n, None, _stream(stream))
+        _check(rc, "qlayer_stack_forward_attn")
     return h
 
 
 def stack_forward_timed(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tensor,
                         events, n_layers: int | None = None, eps: float = 1e-5,
-                        group: int = GROUP, stream=None):
+                        group: int = GROUP, stream=None, attn=None):
     """stack_forward with events: a list of 8 * n_layers torch.cuda.Event
     (enable_timing=True) recorded around each projection launch."""
     _need(h, "h", (torch.float32,), 2)
@@ -243,10 +288,17 @@ def stack_forward_timed(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch
             e.record(st)
     ev_arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
     ws_n = workspace.numel() * workspace.element_size()
-    _check(lib.qlayer_stack_forward_timed(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
-                                          M, d, d_ff, group, eps, _ptr(workspace), ws_n,
-                                          ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st)),
-           "qlayer_stack_forward_timed")
+    if attn is None:
+        rc = lib.qlayer_stack_forward_timed(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
+                                            M, d, d_ff, group, eps, _ptr(workspace), ws_n,
+                                            ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st))
+        _check(rc, "qlayer_stack_forward_timed")
+    else:
+        rc = lib.qlayer_stack_forward_attn(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
+                                           M, d, d_ff, group, eps, _attn_cfg(attn),
+                                           _ptr(workspace), ws_n,
+                                           ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st))
+        _check(rc, "qlayer_stack_forward_attn")
     return h
 
 

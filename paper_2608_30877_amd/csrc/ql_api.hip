@@ -97,7 +97,7 @@ StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   L.qkv = off;
   off += align256((size_t)M * 3 * d * 2);
   L.u = off;
-  off += align256((size_t)M * d_ff * 2);
+  off += align256((size_t)M * kmax * 2);  // u, or the attention output [M][d]
   L.av = off;
   off += L.small ? 0 : align256((size_t)M * d * 2);
   L.ns0 = off;
@@ -106,6 +106,19 @@ StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   off += L.small ? 0 : ns_bytes(M, kmax);
   L.total = off;
   return L;
+}
+
+int check_attention(int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window) {
+  if (M <= 0 || heads <= 0 || seq_len <= 0 || window <= 0) return QL_ERR_ARG;
+  if (M > (1LL << 30) || M % seq_len) return QL_ERR_ARG;
+  if (d != (int64_t)heads * 128) return QL_ERR_UNSUPPORTED;
+  if (attention_tiles(M, heads, seq_len) > 0x7fffffffLL) return QL_ERR_ARG;
+  return QL_OK;
+}
+
+inline bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
 }
 
 }  // namespace
@@ -210,14 +223,34 @@ int qlinear_rmsnorm(const float* h, uint16_t* a, int64_t M, int64_t d, float eps
   return hip_status(launch_rmsnorm(h, a, nullptr, M, d, 0, eps, false, (hipStream_t)stream));
 }
 
-int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* h, int64_t M,
-                               int64_t d, int64_t d_ff, int32_t group, float eps, void* workspace,
-                               size_t ws_bytes, void* const* events, ql_stream_t stream) {
+int qlinear_attention(const uint16_t* qkv, int64_t ldqkv, uint16_t* out, int64_t ldo,
+                      int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window,
+                      ql_stream_t stream) {
+  if (!qkv || !out) return QL_ERR_ARG;
+  int rc = check_attention(M, d, heads, seq_len, window);
+  if (rc) return rc;
+  if (ldqkv < 3 * d || ldo < d) return QL_ERR_ARG;
+  if (!aligned16(qkv) || !aligned16(out) || ldqkv % 8 || ldo % 8) return QL_ERR_ALIGN;
+  if (overlap(qkv, (size_t)((M - 1) * ldqkv + 3 * d) * 2, out, (size_t)((M - 1) * ldo + d) * 2))
+    return QL_ERR_ARG;
+  return hip_status(launch_attention(qkv, ldqkv, out, ldo, M, (int)d, heads, seq_len, window,
+                                     (hipStream_t)stream));
+}
+
+int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h, int64_t M,
+                              int64_t d, int64_t d_ff, int32_t group, float eps,
+                              const ql_attention_cfg* attn, void* workspace, size_t ws_bytes,
+                              void* const* events, ql_stream_t stream) {
   if (!layers || !h || n_layers < 0) return QL_ERR_ARG;
   int rc = check_shape(M, d, d, group);
   if (rc) return rc;
   rc = check_shape(M, d_ff, d_ff, group);
   if (rc) return rc;
+  const bool use_attn = attn && attn->heads != 0;
+  if (use_attn) {
+    rc = check_attention(M, d, attn->heads, attn->seq_len, attn->window);
+    if (rc) return rc;
+  }
   if (!aligned16(h)) return QL_ERR_ALIGN;
   const StackLayout L = stack_layout(M, d, d_ff);
   if (!workspace || ws_bytes < L.total) return QL_ERR_WORKSPACE;
@@ -258,8 +291,16 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
       QL_TRY(mark(l, 0, 0));
       QL_TRY(launch_gemv(a, d, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s));
       QL_TRY(mark(l, 0, 1));
+      const uint16_t* v = qkv + 2 * d;
+      int64_t ldv = 3 * d;
+      if (use_attn) {
+        QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
+                                attn->window, s));
+        v = u;
+        ldv = d;
+      }
       QL_TRY(mark(l, 1, 0));
-      QL_TRY(launch_gemv(qkv + 2 * d, 3 * d, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
+      QL_TRY(launch_gemv(v, ldv, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
       QL_TRY(mark(l, 1, 1));
       QL_TRY(launch_rmsnorm(h, a, nullptr, M, d, 0, eps, false, s));
       QL_TRY(mark(l, 2, 0));
@@ -274,8 +315,13 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
       QL_TRY(launch_rmsnorm(h, a, ns0, M, d, Mp, eps, true, s));
       QL_TRY(mark(l, 0, 0));
       QL_TRY(launch_gemm(a, ns0, Mp, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s,
-                         &vprep));
+                         use_attn ? nullptr : &vprep));
       QL_TRY(mark(l, 0, 1));
+      if (use_attn) {
+        QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
+                                attn->window, s));
+        QL_TRY(launch_prep(u, d, av, ns1, M, d, Mp, s));
+      }
       QL_TRY(mark(l, 1, 0));
       QL_TRY(launch_gemm(av, ns1, Mp, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
       QL_TRY(mark(l, 1, 1));
@@ -293,11 +339,18 @@ int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* 
   return QL_OK;
 }
 
+int qlayer_stack_forward_timed(const ql_layer* layers, int32_t n_layers, float* h, int64_t M,
+                               int64_t d, int64_t d_ff, int32_t group, float eps, void* workspace,
+                               size_t ws_bytes, void* const* events, ql_stream_t stream) {
+  return qlayer_stack_forward_attn(layers, n_layers, h, M, d, d_ff, group, eps, nullptr,
+                                   workspace, ws_bytes, events, stream);
+}
+
 int qlayer_stack_forward(const ql_layer* layers, int32_t n_layers, float* h, int64_t M,
                          int64_t d, int64_t d_ff, int32_t group, float eps, void* workspace,
                          size_t ws_bytes, ql_stream_t stream) {
-  return qlayer_stack_forward_timed(layers, n_layers, h, M, d, d_ff, group, eps, workspace,
-                                    ws_bytes, nullptr, stream);
+  return qlayer_stack_forward_attn(layers, n_layers, h, M, d, d_ff, group, eps, nullptr,
+                                   workspace, ws_bytes, nullptr, stream);
 }
 
 void qlinear_release(void) {

@@ -115,6 +115,15 @@ def ternary_bf16_cuda(seed: int, M: int, K: int):
     return torch.where(t == 0, 0, torch.where(t > 0, 0x3F80, -16512)).to(torch.int16)
 
 
+def qkv_bf16(seed: int, M: int, d: int, std: float = 2.2) -> np.ndarray:
+    """A [Q | K | V] buffer [M, 3d] as bf16 bits, entries N(0, std^2).  The
+    default std is that of a QKV projection output at 175B width
+    (0.02 * sqrt(12288) for unit-RMS inputs and N(0, 0.02) weights)."""
+    z = _rng(seed + 12_000_000).standard_normal((M, 3 * d), dtype=np.float32)
+    z *= np.float32(std)
+    return f32_to_bf16_bits(z)
+
+
 def random_packed_bytes_cuda(seed: int, N: int, K: int):
     """Uniform random code bytes [N, K/2] (uint8) on the current CUDA device."""
     import torch

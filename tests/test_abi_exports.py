@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     for need in ["qlinear_pack", "qlinear_forward", "qlayer_stack_forward", "qlinear_dequant",
                  "qlinear_forward_ex", "qlinear_workspace_bytes", "qlinear_status_string",
                  "qlayer_stack_workspace_bytes", "qlinear_rmsnorm", "qlinear_release",
-                 "qlayer_stack_workspace_offsets"]:
+                 "qlayer_stack_workspace_offsets", "qlinear_attention",
+                 "qlayer_stack_forward_attn"]:
         assert need in names, need
 
 
@@ -100,3 +101,39 @@ def test_stack_errors_without_launch(lib):
     assert f(None, 1, p, 8, 256, 512, 128, 1e-5, p, 1 << 30, None) == 1
     assert f(p, 1, p, 8, 200, 512, 128, 1e-5, p, 1 << 30, None) == 1      # d % 128
     assert f(p, 1, p, 8, 256, 512, 128, 1e-5, p, 16, None) == 6           # workspace
+
+
+def test_attention_errors_without_launch(lib):
+    f = lib.qlinear_attention
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    f.argtypes = [vp, i64, vp, i64, i64, i64, i32, i32, i32, vp]
+    f.restype = ctypes.c_int
+    q, o = ctypes.c_void_p(1 << 20), ctypes.c_void_p(1 << 30)   # never dereferenced
+    assert f(None, 768, o, 256, 128, 256, 2, 64, 8, None) == 1      # null pointer
+    assert f(q, 768, o, 256, 0, 256, 2, 64, 8, None) == 1           # M <= 0
+    assert f(q, 768, o, 256, 128, 256, 2, 100, 8, None) == 1        # M % seq_len
+    assert f(q, 768, o, 256, 128, 256, 2, 64, 0, None) == 1         # window 0
+    assert f(q, 768, o, 256, 128, 256, 2, 0, 8, None) == 1          # seq_len 0
+    assert f(q, 768, o, 256, 128, 384, 2, 64, 8, None) == 2         # head dim 192
+    assert f(q, 700, o, 256, 128, 256, 2, 64, 8, None) == 1         # ldqkv < 3d
+    assert f(q, 772, o, 256, 128, 256, 2, 64, 8, None) == 3         # row stride not 16 B
+    assert f(ctypes.c_void_p((1 << 20) + 8), 768, o, 256, 128, 256, 2, 64, 8, None) == 3
+    # out overlapping qkv
+    assert f(q, 768, ctypes.c_void_p((1 << 20) + 4096), 256, 128, 256, 2, 64, 8, None) == 1
+
+
+def test_stack_attention_errors_without_launch(lib):
+    class Cfg(ctypes.Structure):
+        _fields_ = [("heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                    ("window", ctypes.c_int32)]
+
+    f = lib.qlayer_stack_forward_attn
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i32, vp, i64, i64, i64, i32, ctypes.c_float, vp, vp, sz, vp, vp]
+    f.restype = ctypes.c_int
+    p = ctypes.c_void_p(4096)
+    cfg = lambda *a: ctypes.byref(Cfg(*a))
+    assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(3, 64, 8), p, 1 << 30, None, None) == 2
+    assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 48, 8), p, 1 << 30, None, None) == 1
+    assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 64, -1), p, 1 << 30, None, None) == 1
+    assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 64, 8), p, 16, None, None) == 6
