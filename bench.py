@@ -43,7 +43,8 @@ def log(msg):
 
 # source files each kernel family is built from
 KERNEL_SOURCES = {"k_gemm": ("ql_gemm.hip", "ql_device.h", "ql_internal.h"),
-                  "k_gemv": ("ql_gemv.hip", "ql_device.h", "ql_internal.h")}
+                  "k_gemv": ("ql_gemv.hip", "ql_device.h", "ql_internal.h"),
+                  "k_attn": ("ql_attn.hip", "ql_device.h", "ql_internal.h")}
 
 
 def sources_sha256(family: str) -> str:
@@ -176,7 +177,85 @@ def bench_stack(args, ql, synth, torch):
         "gemm_share_of_step": round(gemm_ms / ms, 4),
         "weight_stream_GBps": round(L * sum(wbytes.values()) / (ms / 1e3) / 1e9, 1),
     }
+    if not args.no_attention:
+        out["with_attention"] = bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d,
+                                                      dff, pairs)
     return out, layers
+
+
+# attention between the QKV and out projections: GPT-3 175B head layout
+# (96 heads of 128), one causal window per 512-token pair (the model's 32K
+# window covers a whole pair)
+ATTN = (96, TOKENS_PER_PAIR, 32768)
+
+
+def bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d, dff, pairs):
+    """The same stack with sliding-window attention in place of the width-1
+    stand-in: whole-step time, and the attention kernel's own time (between
+    the QKV projection's end event and the out projection's start event,
+    which also spans the out projection's operand preparation)."""
+    def step(events=None):
+        h.copy_(h0)
+        if events is None:
+            ql.stack_forward(arr, h, dff, ws, attn=ATTN)
+        else:
+            ql.stack_forward_timed(arr, h, dff, ws, events, attn=ATTN)
+
+    step()
+    torch.cuda.synchronize()
+    steps = max(1, min(args.steps, 2))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(8 * L)] for _ in range(steps)]
+    for ev in evs:
+        for e in ev:
+            e.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    gap = [ev[8 * l + 1].elapsed_time(ev[8 * l + 2]) for ev in evs for l in range(L)]
+    t_attn = sum(gap) / len(gap) * 1e-3
+    heads, seq, _ = ATTN
+    # algorithmic bytes: read Q, K, V once, write O once (bf16)
+    abytes = (3 * d + d) * 2 * M
+    flops = 4 * heads * (M // seq) * (seq * (seq + 1) // 2) * 128   # causal QK^T + PV
+    return {"attention": {"heads": heads, "head_dim": 128, "seq_len": seq, "window": ATTN[2]},
+            "steps": steps, "ms_per_step": round(ms, 3), "pairs_per_s": round(pairs / (ms / 1e3), 4),
+            "attention_kernel": "k_attn", "attention_avg_us_incl_out_prep": round(t_attn * 1e6, 1),
+            "attention_algorithmic_bytes": int(abytes),
+            "attention_GBps": round(abytes / t_attn / 1e9, 1),
+            "attention_frac_hbm_peak": round(abytes / t_attn / 1e9 / PEAK_HBM_GBS, 4),
+            "attention_causal_tflops": round(flops / t_attn / 1e12, 1)}
+
+
+def bench_attention(ql, synth, torch, reps=20):
+    """The attention kernel alone at the stack's shape: 8 pairs x 512 tokens,
+    96 heads of 128, one causal window per pair.  HBM-bound: Q, K, V are read
+    and O written once (algorithmic bytes), 4 * heads * pairs * L(L+1)/2 * 128
+    causal flops."""
+    heads, L, W = ATTN
+    M, d = 8 * L, heads * 128
+    qkv = synth.qkv_bf16_cuda(synth.SEED_STACK, M, d)
+    out = torch.empty((M, d), dtype=torch.bfloat16, device="cuda")
+    for _ in range(3):
+        ql.attention(qkv, heads, L, W, out=out)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        ql.attention(qkv, heads, L, W, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps * 1e-3
+    abytes = (3 * d + d) * 2 * M
+    flops = 4 * heads * (M // L) * (L * (L + 1) // 2) * 128
+    return {"shape": f"M={M} heads={heads} head_dim=128 seq_len={L} window={W}",
+            "kernel": "k_attn", "avg_us": round(t * 1e6, 1),
+            "algorithmic_bytes": int(abytes), "GBps": round(abytes / t / 1e9, 1),
+            "frac_hbm_peak": round(abytes / t / 1e9 / PEAK_HBM_GBS, 4),
+            "causal_tflops": round(flops / t / 1e12, 1),
+            "traffic": measured_traffic("k_attn"), "traffic_unit": "bytes/launch"}
 
 
 def bench_small_batch(ql, synth, torch, reps=50, copies=4):
@@ -278,6 +357,8 @@ def main():
     ap.add_argument("--layers", type=int, default=96)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--no-attention", action="store_true",
+                    help="skip the stack variant with sliding-window attention")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -299,6 +380,8 @@ def main():
         out["small_batch"] = bench_small_batch(ql, synth, torch)
         log("[bench] prefill projections")
         out["prefill"] = bench_prefill(ql, synth, torch)
+        log("[bench] attention kernel")
+        out["attention"] = bench_attention(ql, synth, torch)
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(synth, layers=args.layers)

@@ -124,6 +124,18 @@ def qkv_bf16(seed: int, M: int, d: int, std: float = 2.2) -> np.ndarray:
     return f32_to_bf16_bits(z)
 
 
+def qkv_bf16_cuda(seed: int, M: int, d: int, std: float = 2.2):
+    """qkv_bf16's distribution drawn on the current CUDA device with torch's
+    seeded generator: [M, 3d] bf16 (not the same numbers as the host draw)."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    t = torch.empty((M, 3 * d), dtype=torch.float32, device="cuda")
+    t.normal_(0.0, std, generator=g)
+    return t.to(torch.bfloat16)
+
+
 def random_packed_bytes_cuda(seed: int, N: int, K: int):
     """Uniform random code bytes [N, K/2] (uint8) on the current CUDA device."""
     import torch
