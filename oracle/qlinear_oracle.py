@@ -204,8 +204,8 @@ def stack_layer(h: np.ndarray, layer: dict, group: int = GROUP, eps: float = 1e-
             v = qkv[:, 2d:3d] when attn is None (a sliding window of width 1
             makes attention the identity on V), else
             v = bf16(attention_ref(qkv, d, *attn)) with attn = (heads,
-            seq_len, window) (the paper's model uses sliding-window
-            attention, Sec. 1 / 2);
+            seq_len or the list of sequence lengths, window) (the paper's
+            model uses sliding-window attention, Sec. 1 / 2);
             h1 = fp32(h + v W_o^T);  a2 = RMSNorm(h1);
             u = bf16(GELU(a2 W_up^T));  h2 = fp32(h1 + u W_down^T).
     Returns h2 (and the intermediates when keep=True).
@@ -227,17 +227,19 @@ def stack_layer(h: np.ndarray, layer: dict, group: int = GROUP, eps: float = 1e-
     return h2
 
 
-def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len: int,
-                  window: int) -> np.ndarray:
+def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len, window: int) -> np.ndarray:
     """Causal sliding-window multi-head attention of the paper's decoder
     (sliding-window attention with a 32K window, Sec. 1 contribution 1.1 and
     Sec. 2), fp64 from the given bf16 Q, K, V.
 
     qkv_bits [M, 3d] bf16 bits, columns [Q | K | V]; head h uses columns
-    h*dh .. h*dh+dh-1 of each third, dh = d / heads.  The M tokens are M /
-    seq_len independent sequences (one protein-ligand pair each) of seq_len
-    tokens; token i of a sequence attends to tokens j of the same sequence
-    with i - window < j <= i.  Per head:
+    h*dh .. h*dh+dh-1 of each third, dh = d / heads.  The M tokens are
+    independent sequences (one protein-ligand pair each), stored one after
+    the other: seq_len is either one length (M / seq_len sequences of equal
+    length) or the list of the sequences' lengths (a ragged batch, tokens
+    packed without padding; the lengths sum to M).  Token i of a sequence
+    attends to tokens j of the same sequence with i - window < j <= i.  Per
+    head:
         S = Q K^T / sqrt(dh),  P = softmax over the allowed keys (row-wise),
         O = P V.
     Returns O [M, d] (fp64), heads side by side in the column order of Q.
@@ -245,14 +247,23 @@ def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len: int,
     x = bf16_bits_to_f64(np.asarray(qkv_bits))
     M = x.shape[0]
     dh = d // heads
-    if d % heads or M % seq_len:
-        raise ValueError("d must split into heads and M into whole sequences")
+    if d % heads:
+        raise ValueError("d must split into heads")
+    if np.ndim(seq_len) == 0:
+        if seq_len <= 0 or M % seq_len:
+            raise ValueError("M must split into whole sequences")
+        lengths = [int(seq_len)] * (M // int(seq_len))
+    else:
+        lengths = [int(n) for n in seq_len]
+        if min(lengths) <= 0 or sum(lengths) != M:
+            raise ValueError("sequence lengths must be positive and sum to M")
     out = np.empty((M, d), dtype=np.float64)
-    i = np.arange(seq_len)[:, None]
-    j = np.arange(seq_len)[None, :]
-    allowed = (j <= i) & (j > i - window)
-    for p0 in range(0, M, seq_len):
-        rows = slice(p0, p0 + seq_len)
+    p0 = 0
+    for L in lengths:
+        i = np.arange(L)[:, None]
+        j = np.arange(L)[None, :]
+        allowed = (j <= i) & (j > i - window)
+        rows = slice(p0, p0 + L)
         for hh in range(heads):
             c = slice(hh * dh, (hh + 1) * dh)
             q = x[rows, c]
@@ -262,6 +273,7 @@ def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len: int,
             s = np.where(allowed, s, -np.inf)
             e = np.exp(s - s.max(axis=1, keepdims=True))
             out[rows, c] = (e / e.sum(axis=1, keepdims=True)) @ v
+        p0 += L
     return out
 
 

@@ -363,6 +363,43 @@ def test_attention_zero_keys_is_causal_running_mean():
             np.testing.assert_allclose(out[p * L + i], ref, rtol=0, atol=1e-14)
 
 
+def test_attention_ragged_zero_keys_is_running_mean_per_sequence():
+    """Ragged batch (lengths 3, 1, 5, 2 packed without padding), K = 0: each
+    token averages V over the visible tokens of its own sequence."""
+    rng = np.random.default_rng(15)
+    d, heads, lengths, window = 8, 2, [3, 1, 5, 2], 3
+    M = sum(lengths)
+    bits = _qkv(rng.standard_normal((M, d)), np.zeros((M, d)), rng.standard_normal((M, d)))
+    vr = O.bf16_bits_to_f64(bits[:, 2 * d:])
+    out = O.attention_ref(bits, d, heads, lengths, window)
+    p0 = 0
+    for L in lengths:
+        for i in range(L):
+            lo = max(0, i - window + 1)
+            ref = vr[p0 + lo:p0 + i + 1].mean(axis=0)
+            np.testing.assert_allclose(out[p0 + i], ref, rtol=0, atol=1e-14)
+        p0 += L
+    with pytest.raises(ValueError):
+        O.attention_ref(bits, d, heads, [3, 1, 5], window)      # lengths must sum to M
+
+
+def test_attention_ragged_sequences_are_independent():
+    """Each sequence of a ragged batch gives the same output as on its own
+    (changing one sequence leaves the others bit for bit unchanged)."""
+    rng = np.random.default_rng(16)
+    d, heads, lengths = 8, 1, [4, 7, 2]
+    M = sum(lengths)
+    blocks = [rng.standard_normal((M, d)) for _ in range(3)]
+    base = O.attention_ref(_qkv(*blocks), d, heads, lengths, 100)
+    changed = [b.copy() for b in blocks]
+    for b in changed:
+        b[4:11] = rng.standard_normal((7, d))   # the middle sequence
+    out = O.attention_ref(_qkv(*changed), d, heads, lengths, 100)
+    np.testing.assert_array_equal(out[:4], base[:4])
+    np.testing.assert_array_equal(out[11:], base[11:])
+    assert not np.array_equal(out[4:11], base[4:11])
+
+
 def test_attention_window_one_is_identity_on_v():
     """A window of one token reduces attention to the V slice: the width-1
     stand-in of the linear stack."""
