@@ -218,11 +218,35 @@ int qlinear_attention(const uint16_t* qkv, int64_t ldqkv, uint16_t* out,
                       int64_t ldo, int64_t M, int64_t d, int32_t heads,
                       int32_t seq_len, int32_t window, ql_stream_t stream);
 
+/*
+ * qlinear_attention_varlen -- qlinear_attention over a ragged batch: the
+ * sequences (pairs of different lengths, tokens packed without padding)
+ * occupy rows cu_seqlens[s] .. cu_seqlens[s+1]-1, s < n_seqs.
+ *   cu_seqlens  DEVICE int32 [n_seqs + 1], non-decreasing, cu_seqlens[0] = 0,
+ *               cu_seqlens[n_seqs] = M, every length <= max_seq_len.  The
+ *               host does not read it; offsets that break these rules give
+ *               unspecified results (the kernel clamps them to [0, M], so it
+ *               never reads or writes outside qkv and out).  Empty sequences
+ *               are allowed.  Rows not covered by any sequence are not
+ *               written.
+ *   max_seq_len the longest sequence, >= 1 (sizes the launch).
+ * Other arguments and errors as for qlinear_attention (no M % seq_len rule).
+ */
+int qlinear_attention_varlen(const uint16_t* qkv, int64_t ldqkv, uint16_t* out,
+                             int64_t ldo, int64_t M, int64_t d, int32_t heads,
+                             const int32_t* cu_seqlens, int32_t n_seqs,
+                             int32_t max_seq_len, int32_t window,
+                             ql_stream_t stream);
+
 /* Attention between the QKV and output projections of a stack block. */
 typedef struct {
     int32_t heads;    /* 0 selects the width-1 stand-in v = qkv[:, 2d:3d]   */
-    int32_t seq_len;  /* tokens per sequence (M % seq_len == 0)             */
+    int32_t seq_len;  /* tokens per sequence (M % seq_len == 0), or with
+                         cu_seqlens the longest sequence                    */
     int32_t window;   /* sliding-window width, >= 1                         */
+    int32_t n_seqs;   /* ragged batch: number of sequences in cu_seqlens    */
+    const int32_t* cu_seqlens;  /* NULL: uniform sequences of seq_len; else
+                         DEVICE offsets as for qlinear_attention_varlen     */
 } ql_attention_cfg;
 
 /*

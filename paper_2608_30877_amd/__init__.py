@@ -19,7 +19,7 @@ __all__ = [
     "LIB_PATH", "QLError", "lib", "GROUP", "EPI_NONE", "EPI_GELU", "EPI_RESID_F32",
     "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
-    "stack_forward_timed", "make_layers", "release", "attention",
+    "stack_forward_timed", "make_layers", "release", "attention", "attention_varlen",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
@@ -57,6 +57,8 @@ def _load():
                                                       ctypes.c_float, vp, sz, vp, vp]),
         "qlinear_rmsnorm": (ctypes.c_int, [vp, vp, i64, i64, ctypes.c_float, vp]),
         "qlinear_attention": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, i32, i32, vp]),
+        "qlinear_attention_varlen": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, vp, i32,
+                                                    i32, i32, vp]),
         "qlayer_stack_forward_attn": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
                                                      ctypes.c_float, vp, vp, sz, vp, vp]),
         "qlinear_release": (None, []),
@@ -108,15 +110,23 @@ _BITS16 = (torch.bfloat16, torch.int16, torch.uint16, torch.float16)
 
 class _AttnCfg(ctypes.Structure):
     _fields_ = [("heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
-                ("window", ctypes.c_int32)]
+                ("window", ctypes.c_int32), ("n_seqs", ctypes.c_int32),
+                ("cu_seqlens", ctypes.c_void_p)]
 
 
 def _attn_cfg(attn):
-    """None or (heads, seq_len, window) -> pointer to a ql_attention_cfg (or None)."""
+    """None, (heads, seq_len, window) or (heads, cu_seqlens, max_seq_len,
+    window) with cu_seqlens a CUDA int32 tensor -> pointer to a
+    ql_attention_cfg (or None)."""
     if attn is None:
         return None
-    heads, seq_len, window = (int(v) for v in attn)
-    return ctypes.pointer(_AttnCfg(heads, seq_len, window))
+    if len(attn) == 3:
+        heads, seq_len, window = (int(v) for v in attn)
+        return ctypes.pointer(_AttnCfg(heads, seq_len, window, 0, None))
+    heads, cu, max_len, window = attn
+    _need(cu, "cu_seqlens", (torch.int32,), 1)
+    return ctypes.pointer(_AttnCfg(int(heads), int(max_len), int(window), cu.numel() - 1,
+                                   cu.data_ptr()))
 
 
 class _QLayer(ctypes.Structure):
@@ -228,6 +238,29 @@ def attention(qkv: torch.Tensor, heads: int, seq_len: int, window: int,
     return out
 
 
+def attention_varlen(qkv: torch.Tensor, heads: int, cu_seqlens: torch.Tensor,
+                     max_seq_len: int, window: int, out: torch.Tensor | None = None,
+                     stream=None):
+    """attention() over a ragged batch: sequence s is rows cu_seqlens[s] ..
+    cu_seqlens[s+1]-1 (cu_seqlens: CUDA int32 [n_seqs + 1])."""
+    if not isinstance(qkv, torch.Tensor) or not qkv.is_cuda or qkv.dtype not in _BITS16 \
+            or qkv.dim() != 2 or qkv.stride(1) != 1:
+        raise ValueError("qkv must be a 2-D CUDA bf16 tensor with unit column stride")
+    _need(cu_seqlens, "cu_seqlens", (torch.int32,), 1)
+    M = qkv.shape[0]
+    d = 128 * int(heads)
+    if out is None:
+        out = torch.empty((M, d), dtype=torch.bfloat16, device=qkv.device)
+    if not isinstance(out, torch.Tensor) or not out.is_cuda or out.dtype not in _BITS16 \
+            or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be a 2-D CUDA bf16 tensor with unit column stride")
+    _check(lib.qlinear_attention_varlen(_ptr(qkv), qkv.stride(0), _ptr(out), out.stride(0), M, d,
+                                        int(heads), _ptr(cu_seqlens), cu_seqlens.numel() - 1,
+                                        int(max_seq_len), int(window), _stream(stream)),
+           "qlinear_attention_varlen")
+    return out
+
+
 def stack_workspace_bytes(M: int, d: int, d_ff: int, group: int = GROUP) -> int:
     return int(lib.qlayer_stack_workspace_bytes(M, d, d_ff, group))
 
@@ -255,7 +288,9 @@ def stack_forward(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tenso
                   stream=None, attn=None):
     """Run the linear stack in place on the fp32 residual h [M, d].  attn =
     (heads, seq_len, window) runs sliding-window attention between the QKV
-    and out projections; None runs the width-1 stand-in."""
+    and out projections over uniform sequences, (heads, cu_seqlens,
+    max_seq_len, window) over a ragged batch; None runs the width-1
+    stand-in."""
     _need(h, "h", (torch.float32,), 2)
     M, d = h.shape
     n = len(layers_arr) if n_layers is None else n_layers

@@ -108,11 +108,23 @@ StackLayout stack_layout(int64_t M, int64_t d, int64_t d_ff) {
   return L;
 }
 
-int check_attention(int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window) {
+// seq_len: tokens per sequence (uniform, cu_seqlens null) or the longest
+// sequence (ragged: n_seqs sequences at the offsets cu_seqlens[0..n_seqs])
+int check_attention(int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window,
+                    const int32_t* cu_seqlens, int32_t n_seqs) {
   if (M <= 0 || heads <= 0 || seq_len <= 0 || window <= 0) return QL_ERR_ARG;
-  if (M > (1LL << 30) || M % seq_len) return QL_ERR_ARG;
+  if (M > (1LL << 30)) return QL_ERR_ARG;
   if (d != (int64_t)heads * 128) return QL_ERR_UNSUPPORTED;
-  if (attention_tiles(M, heads, seq_len) > 0x7fffffffLL) return QL_ERR_ARG;
+  int64_t seqs;
+  if (cu_seqlens) {
+    if (n_seqs <= 0) return QL_ERR_ARG;
+    if ((uintptr_t)cu_seqlens & 3u) return QL_ERR_ALIGN;
+    seqs = n_seqs;
+  } else {
+    if (M % seq_len) return QL_ERR_ARG;
+    seqs = M / seq_len;
+  }
+  if (attention_tiles(seqs, heads, seq_len) > 0x7fffffffLL) return QL_ERR_ARG;
   return QL_OK;
 }
 
@@ -223,18 +235,34 @@ int qlinear_rmsnorm(const float* h, uint16_t* a, int64_t M, int64_t d, float eps
   return hip_status(launch_rmsnorm(h, a, nullptr, M, d, 0, eps, false, (hipStream_t)stream));
 }
 
-int qlinear_attention(const uint16_t* qkv, int64_t ldqkv, uint16_t* out, int64_t ldo,
-                      int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window,
-                      ql_stream_t stream) {
+static int attention_common(const uint16_t* qkv, int64_t ldqkv, uint16_t* out, int64_t ldo, int64_t M,
+                     int64_t d, int32_t heads, int32_t seq_len, int32_t window,
+                     const int32_t* cu_seqlens, int32_t n_seqs, hipStream_t stream) {
   if (!qkv || !out) return QL_ERR_ARG;
-  int rc = check_attention(M, d, heads, seq_len, window);
+  int rc = check_attention(M, d, heads, seq_len, window, cu_seqlens, n_seqs);
   if (rc) return rc;
   if (ldqkv < 3 * d || ldo < d) return QL_ERR_ARG;
   if (!aligned16(qkv) || !aligned16(out) || ldqkv % 8 || ldo % 8) return QL_ERR_ALIGN;
   if (overlap(qkv, (size_t)((M - 1) * ldqkv + 3 * d) * 2, out, (size_t)((M - 1) * ldo + d) * 2))
     return QL_ERR_ARG;
   return hip_status(launch_attention(qkv, ldqkv, out, ldo, M, (int)d, heads, seq_len, window,
-                                     (hipStream_t)stream));
+                                     cu_seqlens, n_seqs, stream));
+}
+
+int qlinear_attention(const uint16_t* qkv, int64_t ldqkv, uint16_t* out, int64_t ldo,
+                      int64_t M, int64_t d, int32_t heads, int32_t seq_len, int32_t window,
+                      ql_stream_t stream) {
+  return attention_common(qkv, ldqkv, out, ldo, M, d, heads, seq_len, window, nullptr, 0,
+                          (hipStream_t)stream);
+}
+
+int qlinear_attention_varlen(const uint16_t* qkv, int64_t ldqkv, uint16_t* out, int64_t ldo,
+                             int64_t M, int64_t d, int32_t heads, const int32_t* cu_seqlens,
+                             int32_t n_seqs, int32_t max_seq_len, int32_t window,
+                             ql_stream_t stream) {
+  if (!cu_seqlens) return QL_ERR_ARG;
+  return attention_common(qkv, ldqkv, out, ldo, M, d, heads, max_seq_len, window, cu_seqlens,
+                          n_seqs, (hipStream_t)stream);
 }
 
 int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h, int64_t M,
@@ -248,7 +276,8 @@ int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h
   if (rc) return rc;
   const bool use_attn = attn && attn->heads != 0;
   if (use_attn) {
-    rc = check_attention(M, d, attn->heads, attn->seq_len, attn->window);
+    rc = check_attention(M, d, attn->heads, attn->seq_len, attn->window, attn->cu_seqlens,
+                         attn->n_seqs);
     if (rc) return rc;
   }
   if (!aligned16(h)) return QL_ERR_ALIGN;
@@ -295,7 +324,7 @@ int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h
       int64_t ldv = 3 * d;
       if (use_attn) {
         QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
-                                attn->window, s));
+                                attn->window, attn->cu_seqlens, attn->n_seqs, s));
         v = u;
         ldv = d;
       }
@@ -319,7 +348,7 @@ int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h
       QL_TRY(mark(l, 0, 1));
       if (use_attn) {
         QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
-                                attn->window, s));
+                                attn->window, attn->cu_seqlens, attn->n_seqs, s));
         QL_TRY(launch_prep(u, d, av, ns1, M, d, Mp, s));
       }
       QL_TRY(mark(l, 1, 0));

@@ -31,8 +31,10 @@ constexpr int kBK = 64;   // keys per LDS block
 struct AttnParams {
   const uint16_t* qkv;
   uint16_t* out;
+  const int32_t* cu;  // ragged batch: sequence offsets [n_seqs + 1], else null
   int64_t ldq, ldo;
-  int d, L, W, heads, nqb, tiles;
+  int M, d, L, W, heads, nqb, tiles;  // L: the sequence length (uniform) or
+                                      // the longest sequence (ragged)
   float scale2;  // log2(e) / sqrt(head dim)
 };
 
@@ -90,20 +92,20 @@ struct Staged {
   u32x4 v[2];
 };
 
-__device__ __forceinline__ void load_block(const AttnParams& p, int64_t seq0, int j0, int tid,
-                                           int64_t kcol, int64_t vcol, Staged& st) {
+__device__ __forceinline__ void load_block(const AttnParams& p, int64_t seq0, int L, int j0,
+                                           int tid, int64_t kcol, int64_t vcol, Staged& st) {
   // keys past the sequence end (last block of a ragged sequence) repeat its
   // last row; causality masks them for every real query
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int c = k * kThreads + tid, key = c >> 4, ch = c & 15;
-    const int64_t row = seq0 + min(j0 + key, p.L - 1);
+    const int64_t row = seq0 + min(j0 + key, L - 1);
     st.k[k] = *reinterpret_cast<const u32x4*>(p.qkv + row * p.ldq + kcol + ch * 8);
   }
   const int a2 = tid & 31, ch = tid >> 5;
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    const int64_t row = seq0 + min(j0 + 2 * a2 + r, p.L - 1);
+    const int64_t row = seq0 + min(j0 + 2 * a2 + r, L - 1);
     st.v[r] = *reinterpret_cast<const u32x4*>(p.qkv + row * p.ldq + vcol + ch * 8);
   }
 }
@@ -149,17 +151,30 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
   // within a (sequence, head) the longest query blocks come first
   const int ph = t / p.nqb, qb = p.nqb - 1 - (t - ph * p.nqb);
   const int pair = ph / p.heads, head = ph - pair * p.heads;
-  const int64_t seq0 = (int64_t)pair * p.L;
   const int i0 = qb * kBQ;
+  // the sequence's first row and length; ragged offsets are clamped into
+  // [0, M] and the length to the launch's query blocks, so malformed offsets
+  // give wrong results but no access outside the buffers
+  int64_t seq0;
+  int L;
+  if (p.cu) {
+    const int a = min(max(p.cu[pair], 0), p.M), b = min(max(p.cu[pair + 1], a), p.M);
+    seq0 = a;
+    L = min(b - a, p.nqb * kBQ);
+  } else {
+    seq0 = (int64_t)pair * p.L;
+    L = p.L;
+  }
+  if (i0 >= L) return;  // the whole workgroup, before any barrier
   const int64_t qcol = (int64_t)head * kDh, kcol = p.d + qcol, vcol = 2 * (int64_t)p.d + qcol;
 
   // this wave's queries qw0 .. qw1 (wave-uniform); the lane's query iq is the
   // column operand of S^T: chunks 4h + s of its row
-  const int qw0 = i0 + wave * 16, qw1 = min(qw0 + 15, p.L - 1);
+  const int qw0 = i0 + wave * 16, qw1 = min(qw0 + 15, L - 1);
   const int iq = qw0 + lr;
   bf16x8 qf[4];
   {
-    const uint16_t* src = p.qkv + (seq0 + min(iq, p.L - 1)) * p.ldq + qcol;
+    const uint16_t* src = p.qkv + (seq0 + min(iq, L - 1)) * p.ldq + qcol;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
       qf[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + (h * 4 + s) * 8));
@@ -175,20 +190,20 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
   constexpr float kLazy = 8.0f;
   float m = -1e30f, l = 0.f;
 
-  const int ilast = min(i0 + kBQ, p.L) - 1;  // last real query of the workgroup
+  const int ilast = min(i0 + kBQ, L) - 1;  // last real query of the workgroup
   const int kb_lo = max(0, i0 - p.W + 1) / kBK, kb_hi = ilast / kBK;
   uint32_t* sV1 = reinterpret_cast<uint32_t*>(sV);
   Staged st;
-  load_block(p, seq0, kb_lo * kBK, tid, kcol, vcol, st);
+  load_block(p, seq0, L, kb_lo * kBK, tid, kcol, vcol, st);
   for (int kb = kb_lo; kb <= kb_hi; ++kb) {
     const int j0 = kb * kBK;
     __syncthreads();  // the previous block's reads are done
     store_block(st, tid, sK, sV1);
     __syncthreads();
-    if (kb < kb_hi) load_block(p, seq0, j0 + kBK, tid, kcol, vcol, st);
+    if (kb < kb_hi) load_block(p, seq0, L, j0 + kBK, tid, kcol, vcol, st);
 
     // skip blocks no query of this wave can see (wave-uniform)
-    if (qw0 >= p.L || j0 > qw1 || qw0 - (j0 + kBK - 1) >= p.W) continue;
+    if (qw0 >= L || j0 > qw1 || qw0 - (j0 + kBK - 1) >= p.W) continue;
     const bool full = j0 + kBK - 1 <= qw0 && qw1 - j0 < p.W;
 
     // S^T, 4 fragments of 16 keys: lane holds keys j0 + 16 kf + 4 h + r of query iq
@@ -265,7 +280,7 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
 
   // O^T: lane holds query iq (column lr), dims 16 df + 4 h + r
   const float inv = 1.0f / sum_over_h(l);
-  if (iq >= p.L) return;
+  if (iq >= L) return;
   uint16_t* dst = p.out + (seq0 + iq) * p.ldo + qcol;
 #pragma unroll
   for (int df = 0; df < 8; ++df)
@@ -276,23 +291,27 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
 
 }  // namespace
 
-int64_t attention_tiles(int64_t M, int heads, int seq_len) {
-  return (M / seq_len) * heads * ((seq_len + kBQ - 1) / kBQ);
+int64_t attention_tiles(int64_t n_seqs, int heads, int max_len) {
+  return n_seqs * heads * ((max_len + kBQ - 1) / kBQ);
 }
 
 hipError_t launch_attention(const uint16_t* qkv, int64_t ldq, uint16_t* out, int64_t ldo,
-                            int64_t M, int d, int heads, int seq_len, int window, hipStream_t s) {
+                            int64_t M, int d, int heads, int seq_len, int window,
+                            const int32_t* cu_seqlens, int n_seqs, hipStream_t s) {
   AttnParams p;
   p.qkv = qkv;
   p.out = out;
+  p.cu = cu_seqlens;
   p.ldq = ldq;
   p.ldo = ldo;
+  p.M = (int)M;
   p.d = d;
   p.L = seq_len;
   p.W = window;
   p.heads = heads;
   p.nqb = (seq_len + kBQ - 1) / kBQ;
-  p.tiles = (int)attention_tiles(M, heads, seq_len);
+  const int64_t seqs = cu_seqlens ? n_seqs : M / seq_len;
+  p.tiles = (int)attention_tiles(seqs, heads, seq_len);
   p.scale2 = 1.4426950408889634f / sqrtf((float)kDh);
   hipLaunchKernelGGL(k_attn, dim3((unsigned)p.tiles), dim3(kThreads), 0, s, p);
   return hipGetLastError();

@@ -72,11 +72,13 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
                        void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
                        hipStream_t s);
 
-// Causal sliding-window attention over a [Q | K | V] buffer, head dim 128;
-// M = whole sequences of seq_len tokens.  Launches attention_tiles(...)
-// workgroups of 64 queries.
-int64_t attention_tiles(int64_t M, int heads, int seq_len);
+// Causal sliding-window attention over a [Q | K | V] buffer, head dim 128.
+// Uniform batch (cu_seqlens null): M = whole sequences of seq_len tokens.
+// Ragged batch: n_seqs sequences at the device offsets cu_seqlens[0..n_seqs],
+// each at most seq_len tokens.  Launches attention_tiles(...) workgroups.
+int64_t attention_tiles(int64_t n_seqs, int heads, int max_len);
 hipError_t launch_attention(const uint16_t* qkv, int64_t ldq, uint16_t* out, int64_t ldo,
-                            int64_t M, int d, int heads, int seq_len, int window, hipStream_t s);
+                            int64_t M, int d, int heads, int seq_len, int window,
+                            const int32_t* cu_seqlens, int n_seqs, hipStream_t s);
 
 }  // namespace ql

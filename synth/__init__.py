@@ -136,6 +136,15 @@ def qkv_bf16_cuda(seed: int, M: int, d: int, std: float = 2.2):
     return t.to(torch.bfloat16)
 
 
+def pair_lengths(seed: int, n: int, protein=(380, 450), ligand=(40, 62)) -> np.ndarray:
+    """Token counts of n protein-ligand pairs for a ragged (unpadded) batch:
+    residue tokens uniform in `protein` plus ligand tokens uniform in
+    `ligand` (inclusive), so at most 512 with the defaults."""
+    rng = _rng(seed + 13_000_000)
+    return (rng.integers(protein[0], protein[1] + 1, size=n)
+            + rng.integers(ligand[0], ligand[1] + 1, size=n)).astype(np.int64)
+
+
 def random_packed_bytes_cuda(seed: int, N: int, K: int):
     """Uniform random code bytes [N, K/2] (uint8) on the current CUDA device."""
     import torch

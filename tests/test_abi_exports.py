@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
                  "qlinear_forward_ex", "qlinear_workspace_bytes", "qlinear_status_string",
                  "qlayer_stack_workspace_bytes", "qlinear_rmsnorm", "qlinear_release",
                  "qlayer_stack_workspace_offsets", "qlinear_attention",
-                 "qlayer_stack_forward_attn"]:
+                 "qlayer_stack_forward_attn", "qlinear_attention_varlen"]:
         assert need in names, need
 
 
@@ -137,3 +137,16 @@ def test_stack_attention_errors_without_launch(lib):
     assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 48, 8), p, 1 << 30, None, None) == 1
     assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 64, -1), p, 1 << 30, None, None) == 1
     assert f(p, 1, p, 64, 256, 512, 128, 1e-5, cfg(2, 64, 8), p, 16, None, None) == 6
+
+
+def test_attention_varlen_errors_without_launch(lib):
+    f = lib.qlinear_attention_varlen
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    f.argtypes = [vp, i64, vp, i64, i64, i64, i32, vp, i32, i32, i32, vp]
+    f.restype = ctypes.c_int
+    q, o, cu = ctypes.c_void_p(1 << 20), ctypes.c_void_p(1 << 30), ctypes.c_void_p(1 << 12)
+    assert f(q, 768, o, 256, 100, 256, 2, None, 3, 64, 8, None) == 1     # no offsets
+    assert f(q, 768, o, 256, 100, 256, 2, cu, 0, 64, 8, None) == 1       # no sequences
+    assert f(q, 768, o, 256, 100, 256, 2, cu, 3, 0, 8, None) == 1        # max length 0
+    assert f(q, 768, o, 256, 100, 256, 2, ctypes.c_void_p((1 << 12) + 2), 3, 64, 8, None) == 3
+    assert f(q, 768, o, 256, 100, 384, 2, cu, 3, 64, 8, None) == 2       # head dim 192

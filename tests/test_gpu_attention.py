@@ -140,6 +140,62 @@ def test_attention_argument_errors(ql):
     assert e.value.code == 1
 
 
+# ---- ragged batches (pairs of different lengths, no padding) -----------------
+
+def _cu(lengths):
+    return torch.tensor(np.concatenate([[0], np.cumsum(lengths)]), dtype=torch.int32,
+                        device="cuda")
+
+
+@pytest.mark.parametrize("lengths,heads,W", [
+    ([512, 300, 1, 129, 64, 450], 2, 32768),
+    ([7, 130, 0, 255, 128, 3], 1, 100),       # an empty sequence, block-edge lengths
+    ([1, 1, 1, 1], 3, 1),
+    ([200], 2, 65),
+])
+def test_attention_varlen_parity(ql, lengths, heads, W):
+    d = 128 * heads
+    M = int(sum(lengths))
+    say(f"attention varlen lengths={lengths} heads={heads} W={W}")
+    qkv = synth.qkv_bf16(300 + M + W, M, d)
+    out = ql.attention_varlen(dev_u16(qkv), heads, _cu(lengths), max(lengths), W)
+    torch.cuda.synchronize()
+    _check(host_u16(out), qkv, d, heads, [n for n in lengths if n], W)
+
+
+def test_attention_varlen_uniform_matches_uniform_kernel(ql):
+    """Equal lengths given as offsets run the same arithmetic: bit-equal."""
+    M, heads, L, W = 1024, 2, 256, 300
+    d = 128 * heads
+    qkv = dev_u16(synth.qkv_bf16(13, M, d))
+    a = ql.attention(qkv, heads, L, W)
+    b = ql.attention_varlen(qkv, heads, _cu([L] * (M // L)), L, W)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_attention_varlen_full_width_sampled(ql):
+    """175B width, 96 heads: a ragged batch of 9 pairs (380-450 residue plus
+    40-62 ligand tokens each, packed without padding); five sampled (pair,
+    head) blocks against the oracle."""
+    heads, W = 96, 32768
+    d = 128 * heads
+    lengths = synth.pair_lengths(synth.SEED_STACK, 9)
+    M = int(lengths.sum())
+    say(f"attention varlen full width M={M}")
+    qkv = synth.qkv_bf16(synth.SEED_STACK + 2, M, d)
+    out = host_u16(ql.attention_varlen(dev_u16(qkv), heads, _cu(lengths), int(lengths.max()), W))
+    starts = np.concatenate([[0], np.cumsum(lengths)])
+    rng = np.random.default_rng(22)
+    for _ in range(5):
+        pr, hh = int(rng.integers(len(lengths))), int(rng.integers(heads))
+        rows = slice(starts[pr], starts[pr + 1])
+        cols = np.concatenate([np.arange(hh * 128, hh * 128 + 128) + t * d for t in range(3)])
+        sub = np.ascontiguousarray(qkv[rows][:, cols])
+        got = out[rows, hh * 128:hh * 128 + 128].copy()
+        _check(got, sub, 128, 1, int(lengths[pr]), W)
+
+
 # ---- the stack with attention -------------------------------------------
 
 def _packed_layer_oracle(seed, layer, d, dff):
@@ -222,4 +278,26 @@ def test_full_width_block_with_attention_sampled_sequence(ql):
     ref = O.stack_layer(h0[rows], layer, attn=(96, L, W)).astype(np.float64)
     err = O.rel_fro(got - h0[rows], ref - h0[rows])
     say(f"  rel err of the residual update: {err:.3e}")
+    assert err <= 5e-3
+
+
+@pytest.mark.parametrize("lengths", [[5, 3, 8], [40, 1, 77, 8], [130, 70, 120, 50]])
+def test_small_stack_with_ragged_attention(ql, lengths):
+    """4 blocks at d = 256 on a ragged batch (small-batch kernels for 16
+    tokens, MFMA above): attention over each pair's own tokens only."""
+    d, dff, nl, heads, W = 256, 1024, 4, 2, 32768
+    M = sum(lengths)
+    say(f"stack+ragged attention lengths={lengths}")
+    layers = [_packed_layer_oracle(52, l, d, dff) for l in range(nl)]
+    h0 = synth.residual_f32(52 + M, M, d)
+    ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
+    h = dev(h0)
+    ql.stack_forward(ql.make_layers([_to_dev(x) for x in layers]), h, dff, ws,
+                     attn=(heads, _cu(lengths), max(lengths), W))
+    torch.cuda.synchronize()
+    ref = h0
+    for x in layers:
+        ref = O.stack_layer(ref, x, attn=(heads, lengths, W))
+    err = O.rel_fro(h.cpu().numpy().astype(np.float64) - h0, ref.astype(np.float64) - h0)
+    say(f"  end-to-end rel err of the residual update: {err:.3e}")
     assert err <= 5e-3
