@@ -180,6 +180,9 @@ def bench_stack(args, ql, synth, torch):
     if not args.no_attention:
         out["with_attention"] = bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d,
                                                       dff, pairs)
+        out["ragged"] = bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M, d, dff)
+        out["ragged"]["vs_padded_with_attention"] = round(
+            out["ragged"]["pairs_per_s"] / out["with_attention"]["pairs_per_s"], 4)
     return out, layers
 
 
@@ -227,6 +230,35 @@ def bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d, dff, pairs):
             "attention_GBps": round(abytes / t_attn / 1e9, 1),
             "attention_frac_hbm_peak": round(abytes / t_attn / 1e9 / PEAK_HBM_GBS, 4),
             "attention_causal_tflops": round(flops / t_attn / 1e12, 1)}
+
+
+def bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M_budget, d, dff):
+    """Continuous batching without padding: whole pairs of their own lengths
+    (380-450 residue + 40-62 ligand tokens, seeded) packed into the same
+    4096-token budget, attention over each pair's own tokens."""
+    lengths = synth.pair_lengths(synth.SEED_STACK, 64)
+    n = int((lengths.cumsum() <= M_budget).sum())
+    lengths = lengths[:n]
+    M = int(lengths.sum())
+    cu = torch.tensor([0] + list(lengths.cumsum()), dtype=torch.int32, device="cuda")
+    attn = (ATTN[0], cu, int(lengths.max()), ATTN[2])
+    hr = h0[:M].clone()
+
+    def step():
+        hr.copy_(h0[:M])
+        ql.stack_forward(arr, hr, dff, ws, attn=attn)
+
+    step()
+    torch.cuda.synchronize()
+    steps = max(1, min(args.steps, 2))
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"pairs": n, "tokens": M, "padded_tokens": n * TOKENS_PER_PAIR,
+            "lengths": "380-450 residue + 40-62 ligand tokens per pair (seeded)",
+            "steps": steps, "ms_per_step": round(ms, 3), "pairs_per_s": round(n / (ms / 1e3), 4)}
 
 
 def bench_attention(ql, synth, torch, reps=20):
