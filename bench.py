@@ -183,6 +183,9 @@ def bench_stack(args, ql, synth, torch):
         out["ragged"] = bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M, d, dff)
         out["ragged"]["vs_padded_with_attention"] = round(
             out["ragged"]["pairs_per_s"] / out["with_attention"]["pairs_per_s"], 4)
+    if not args.no_streamed:
+        out["host_streamed"] = bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d,
+                                                    dff, pairs, ms)
     return out, layers
 
 
@@ -230,6 +233,57 @@ def bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d, dff, pairs):
             "attention_GBps": round(abytes / t_attn / 1e9, 1),
             "attention_frac_hbm_peak": round(abytes / t_attn / 1e9 / PEAK_HBM_GBS, 4),
             "attention_causal_tflops": round(flops / t_attn / 1e12, 1)}
+
+
+STREAM_POOL = 16   # distinct blocks kept in page-locked host memory for the streamed variant
+
+
+def bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d, dff, pairs, resident_ms):
+    """The weights in page-locked host memory instead of HBM, copied block by
+    block into two device slots while the previous block computes (the
+    paper's host paging, with prefetch).  STREAM_POOL distinct blocks are
+    copied to the host (15 GB) and stand for the 96 in turn: every one of
+    the 96 blocks' bytes crosses PCIe in every step."""
+    pool = []
+    for l in range(min(STREAM_POOL, L)):
+        pool.append({k: (q.cpu().pin_memory(), s.cpu().pin_memory())
+                     for k, (q, s) in layers[l].items()})
+    host_arr = ql.make_layers([pool[l % len(pool)] for l in range(L)])
+    slot = ql.stack_slot_bytes(d, dff)
+    slots = torch.empty(2 * slot, dtype=torch.uint8, device="cuda")
+    cs = torch.cuda.Stream()
+
+    def step():
+        h.copy_(h0)
+        ql.stack_forward_streamed(host_arr, h, dff, ws, slots, cs)
+
+    step()
+    torch.cuda.synchronize()
+    steps = max(1, min(args.steps, 2))
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    # the copy alone: one block's eight arrays host -> slot, back to back
+    blk = sum(q.numel() + 2 * s.numel() for q, s in pool[0].values())
+    flat = torch.empty(blk, dtype=torch.uint8).pin_memory()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(cs):
+        for _ in range(2):
+            slots[:blk].copy_(flat, non_blocking=True)
+        e0.record(cs)
+        for _ in range(8):
+            slots[:blk].copy_(flat, non_blocking=True)
+        e1.record(cs)
+    torch.cuda.synchronize()
+    h2d = blk / (e0.elapsed_time(e1) / 8 * 1e-3) / 1e9
+    copy_ms = L * blk / (h2d * 1e9) * 1e3
+    return {"pool_blocks": len(pool), "block_bytes": int(blk), "ms_per_step": round(ms, 3),
+            "pairs_per_s": round(pairs / (ms / 1e3), 4),
+            "h2d_GBps": round(h2d, 1), "copy_ms_per_step_alone": round(copy_ms, 1),
+            "resident_ms_per_step": round(resident_ms, 3),
+            "overlap_efficiency": round(max(copy_ms, resident_ms) / ms, 4)}
 
 
 def bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M_budget, d, dff):
@@ -390,7 +444,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-attention", action="store_true",
-                    help="skip the stack variant with sliding-window attention")
+                    help="skip the stack variants with sliding-window attention")
+    ap.add_argument("--no-streamed", action="store_true",
+                    help="skip the variant with the weights streamed from host memory")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "

@@ -265,6 +265,39 @@ int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h
                               void* workspace, size_t ws_bytes,
                               void* const* events, ql_stream_t stream);
 
+/* Bytes of one weight slot of qlayer_stack_forward_streamed (a block's four
+ * packed matrices, each codes + scales 256-byte aligned); the call needs two. */
+size_t qlayer_stack_slot_bytes(int64_t d, int64_t d_ff, int32_t group);
+
+/*
+ * qlayer_stack_forward_streamed -- qlayer_stack_forward_attn for weights
+ * that stay in HOST memory: the paper keeps its weights in host RAM and
+ * schedules their loading around the computation (adaptive memory
+ * management, Sec. 3.1; page swapping is 72 % of its runtime, Sec. 4.3;
+ * prefetching is its stated next step, Sec. 5).  Here the pages are whole
+ * blocks, double-buffered: while block l computes from one device
+ * slot on `stream`, block l+1's eight arrays are copied into the other slot
+ * with hipMemcpyAsync on `copy_stream`, ordered by events (a copy into a
+ * slot waits until the block that read it has finished; a block waits for
+ * its copy).  The step is bound by max(copy, compute) instead of their sum.
+ *   host_layers  HOST array of ql_layer structs whose qweight / scales are
+ *                page-locked HOST memory (hipHostMalloc); pageable memory is
+ *                refused (QL_ERR_ARG) because its copies would not overlap.
+ *   slots        DEVICE buffer of >= 2 * qlayer_stack_slot_bytes(d, d_ff, g)
+ *                bytes, 256-byte aligned (QL_ERR_WORKSPACE / QL_ERR_ALIGN).
+ *   copy_stream  a stream other than `stream` (QL_ERR_ARG otherwise); keep
+ *                both at the default priority.
+ * h, workspace, attn as for qlayer_stack_forward_attn.  Returns after
+ * enqueuing; the host arrays and the slots must stay valid until `stream`
+ * has completed the call's work.  Calls that overlap on one slot buffer race.
+ */
+int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
+                                  float* h, int64_t M, int64_t d, int64_t d_ff,
+                                  int32_t group, float eps,
+                                  const ql_attention_cfg* attn, void* workspace,
+                                  size_t ws_bytes, void* slots, size_t slot_bytes,
+                                  ql_stream_t stream, ql_stream_t copy_stream);
+
 /* Host: byte offsets of the qkv and u buffers inside the stack workspace. */
 void qlayer_stack_workspace_offsets(int64_t M, int64_t d, int64_t d_ff,
                                     int32_t group, size_t* qkv_off,

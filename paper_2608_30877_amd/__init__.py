@@ -20,6 +20,7 @@ __all__ = [
     "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
     "stack_forward_timed", "make_layers", "release", "attention", "attention_varlen",
+    "stack_slot_bytes", "stack_forward_streamed",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
@@ -56,6 +57,10 @@ def _load():
         "qlayer_stack_forward_timed": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
                                                       ctypes.c_float, vp, sz, vp, vp]),
         "qlinear_rmsnorm": (ctypes.c_int, [vp, vp, i64, i64, ctypes.c_float, vp]),
+        "qlayer_stack_slot_bytes": (sz, [i64, i64, i32]),
+        "qlayer_stack_forward_streamed": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
+                                                         ctypes.c_float, vp, vp, sz, vp, sz, vp,
+                                                         vp]),
         "qlinear_attention": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, i32, i32, vp]),
         "qlinear_attention_varlen": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, vp, i32,
                                                     i32, i32, vp]),
@@ -334,6 +339,31 @@ def stack_forward_timed(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch
                                            _ptr(workspace), ws_n,
                                            ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st))
         _check(rc, "qlayer_stack_forward_attn")
+    return h
+
+
+def stack_slot_bytes(d: int, d_ff: int, group: int = GROUP) -> int:
+    return int(lib.qlayer_stack_slot_bytes(d, d_ff, group))
+
+
+def stack_forward_streamed(host_layers_arr, h: torch.Tensor, d_ff: int, workspace: torch.Tensor,
+                           slots: torch.Tensor, copy_stream, n_layers: int | None = None,
+                           eps: float = 1e-5, group: int = GROUP, stream=None, attn=None):
+    """stack_forward with the packed weights in page-locked host memory
+    (make_layers over pinned CPU tensors), copied block by block into the two
+    device slots of `slots` (uint8 CUDA tensor of 2 * stack_slot_bytes) on
+    `copy_stream` while the previous block computes on `stream`.  Keep the
+    host tensors and slots alive until `stream` has finished."""
+    _need(h, "h", (torch.float32,), 2)
+    M, d = h.shape
+    n = len(host_layers_arr) if n_layers is None else n_layers
+    ws_n = workspace.numel() * workspace.element_size()
+    sl_n = slots.numel() * slots.element_size()
+    rc = lib.qlayer_stack_forward_streamed(ctypes.cast(host_layers_arr, ctypes.c_void_p), n,
+                                           _ptr(h), M, d, d_ff, group, eps, _attn_cfg(attn),
+                                           _ptr(workspace), ws_n, _ptr(slots), sl_n,
+                                           _stream(stream), _stream(copy_stream))
+    _check(rc, "qlayer_stack_forward_streamed")
     return h
 
 

@@ -133,6 +133,182 @@ inline bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// ---- stack driver
+struct StackRun {
+  float* h;
+  int64_t M, d, d_ff, Mp;
+  float eps;
+  const ql_attention_cfg* attn;  // null: the width-1 stand-in
+  bool small;                    // every projection runs the small-batch kernel
+  uint16_t *a, *qkv, *u, *av;
+  float *ns0, *ns1;
+  void* const* events;
+  hipStream_t s;
+};
+
+int stack_setup(float* h, int64_t M, int64_t d, int64_t d_ff, int32_t group, float eps,
+                const ql_attention_cfg* attn, void* workspace, size_t ws_bytes,
+                void* const* events, hipStream_t s, StackRun* r) {
+  if (!h) return QL_ERR_ARG;
+  int rc = check_shape(M, d, d, group);
+  if (rc) return rc;
+  rc = check_shape(M, d_ff, d_ff, group);
+  if (rc) return rc;
+  const bool use_attn = attn && attn->heads != 0;
+  if (use_attn) {
+    rc = check_attention(M, d, attn->heads, attn->seq_len, attn->window, attn->cu_seqlens,
+                         attn->n_seqs);
+    if (rc) return rc;
+  }
+  if (!aligned16(h)) return QL_ERR_ALIGN;
+  const StackLayout L = stack_layout(M, d, d_ff);
+  if (!workspace || ws_bytes < L.total) return QL_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return QL_ERR_ALIGN;
+  char* ws = static_cast<char*>(workspace);
+  *r = StackRun{h, M, d, d_ff, padded_rows(M), eps, use_attn ? attn : nullptr, L.small,
+                reinterpret_cast<uint16_t*>(ws + L.a), reinterpret_cast<uint16_t*>(ws + L.qkv),
+                reinterpret_cast<uint16_t*>(ws + L.u), reinterpret_cast<uint16_t*>(ws + L.av),
+                reinterpret_cast<float*>(ws + L.ns0), reinterpret_cast<float*>(ws + L.ns1),
+                events, s};
+  return QL_OK;
+}
+
+int check_layer(const ql_layer& Ly) {
+  const ql_qmat* mats[4] = {&Ly.qkv, &Ly.out, &Ly.up, &Ly.down};
+  for (const ql_qmat* q : mats) {
+    if (!q->qweight || !q->scales) return QL_ERR_ARG;
+    if (!aligned16(q->qweight) || ((uintptr_t)q->scales & 1u)) return QL_ERR_ALIGN;
+  }
+  return QL_OK;
+}
+
+// optional timing hook: events[8l + 2j] / [8l + 2j + 1] bracket projection j
+inline hipError_t mark(const StackRun& r, int l, int j, int end) {
+  if (!r.events) return hipSuccess;
+  void* ev = r.events[8 * l + 2 * j + end];
+  return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), r.s) : hipSuccess;
+}
+
+// One block on the residual stream (asynchronous on r.s).
+hipError_t run_block(const StackRun& r, const ql_layer& Ly, int l) {
+  const int64_t M = r.M, d = r.d, d_ff = r.d_ff, Mp = r.Mp;
+  const ql_attention_cfg* at = r.attn;
+  hipStream_t s = r.s;
+  hipError_t e = hipSuccess;
+#define QL_TRY(call)                  \
+  do {                                \
+    e = (call);                       \
+    if (e != hipSuccess) return e;    \
+  } while (0)
+  if (r.small) {
+    QL_TRY(launch_rmsnorm(r.h, r.a, nullptr, M, d, 0, r.eps, false, s));
+    QL_TRY(mark(r, l, 0, 0));
+    QL_TRY(launch_gemv(r.a, d, Ly.qkv.qweight, Ly.qkv.scales, r.qkv, 3 * d, M, 3 * d, d, 0, s));
+    QL_TRY(mark(r, l, 0, 1));
+    const uint16_t* v = r.qkv + 2 * d;
+    int64_t ldv = 3 * d;
+    if (at) {
+      QL_TRY(launch_attention(r.qkv, 3 * d, r.u, d, M, (int)d, at->heads, at->seq_len, at->window,
+                              at->cu_seqlens, at->n_seqs, s));
+      v = r.u;
+      ldv = d;
+    }
+    QL_TRY(mark(r, l, 1, 0));
+    QL_TRY(launch_gemv(v, ldv, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2, s));
+    QL_TRY(mark(r, l, 1, 1));
+    QL_TRY(launch_rmsnorm(r.h, r.a, nullptr, M, d, 0, r.eps, false, s));
+    QL_TRY(mark(r, l, 2, 0));
+    QL_TRY(launch_gemv(r.a, d, Ly.up.qweight, Ly.up.scales, r.u, d_ff, M, d_ff, d, 1, s));
+    QL_TRY(mark(r, l, 2, 1));
+    QL_TRY(mark(r, l, 3, 0));
+    QL_TRY(launch_gemv(r.u, d_ff, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2, s));
+    QL_TRY(mark(r, l, 3, 1));
+  } else {
+    const GemmPrep vprep{r.av, d, r.ns1, 2 * d};  // V slice -> out-projection operand
+    const GemmPrep uprep{r.u, d_ff, r.ns1, 0};    // GELU output -> down-projection operand
+    QL_TRY(launch_rmsnorm(r.h, r.a, r.ns0, M, d, Mp, r.eps, true, s));
+    QL_TRY(mark(r, l, 0, 0));
+    QL_TRY(launch_gemm(r.a, r.ns0, Mp, Ly.qkv.qweight, Ly.qkv.scales, r.qkv, 3 * d, M, 3 * d, d,
+                       0, s, at ? nullptr : &vprep));
+    QL_TRY(mark(r, l, 0, 1));
+    if (at) {
+      QL_TRY(launch_attention(r.qkv, 3 * d, r.u, d, M, (int)d, at->heads, at->seq_len, at->window,
+                              at->cu_seqlens, at->n_seqs, s));
+      QL_TRY(launch_prep(r.u, d, r.av, r.ns1, M, d, Mp, s));
+    }
+    QL_TRY(mark(r, l, 1, 0));
+    QL_TRY(launch_gemm(r.av, r.ns1, Mp, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2, s));
+    QL_TRY(mark(r, l, 1, 1));
+    QL_TRY(launch_rmsnorm(r.h, r.a, r.ns0, M, d, Mp, r.eps, true, s));
+    QL_TRY(mark(r, l, 2, 0));
+    QL_TRY(launch_gemm(r.a, r.ns0, Mp, Ly.up.qweight, Ly.up.scales, nullptr, d_ff, M, d_ff, d, 1,
+                       s, &uprep));
+    QL_TRY(mark(r, l, 2, 1));
+    QL_TRY(mark(r, l, 3, 0));
+    QL_TRY(launch_gemm(r.u, r.ns1, Mp, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2, s));
+    QL_TRY(mark(r, l, 3, 1));
+  }
+#undef QL_TRY
+  return hipSuccess;
+}
+
+// ---- host-streamed weights: one block's four matrices in a device slot
+struct SlotLayout {
+  size_t q[4], sc[4], total;  // byte offsets of codes and scales: qkv, out, up, down
+  int64_t n[4], k[4];         // matrix shapes
+};
+
+SlotLayout slot_layout(int64_t d, int64_t d_ff) {
+  SlotLayout S;
+  const int64_t n[4] = {3 * d, d, d_ff, d}, k[4] = {d, d, d, d_ff};
+  size_t off = 0;
+  for (int i = 0; i < 4; ++i) {
+    S.n[i] = n[i];
+    S.k[i] = k[i];
+    S.q[i] = off;
+    off += align256((size_t)n[i] * k[i] / 2);
+    S.sc[i] = off;
+    off += align256((size_t)n[i] * (k[i] / kGroup) * 2);
+  }
+  S.total = off;
+  return S;
+}
+
+ql_layer slot_layer(char* base, const SlotLayout& S) {
+  ql_qmat m[4];
+  for (int i = 0; i < 4; ++i)
+    m[i] = ql_qmat{reinterpret_cast<const uint8_t*>(base + S.q[i]),
+                   reinterpret_cast<const uint16_t*>(base + S.sc[i])};
+  return ql_layer{m[0], m[1], m[2], m[3]};
+}
+
+hipError_t copy_matrices(const ql_layer& src, const ql_layer& dst, int64_t d, int64_t d_ff,
+                         hipStream_t cs) {
+  const SlotLayout S = slot_layout(d, d_ff);
+  const ql_qmat* a[4] = {&src.qkv, &src.out, &src.up, &src.down};
+  const ql_qmat* b[4] = {&dst.qkv, &dst.out, &dst.up, &dst.down};
+  for (int i = 0; i < 4; ++i) {
+    hipError_t e = hipMemcpyAsync(const_cast<uint8_t*>(b[i]->qweight), a[i]->qweight,
+                                  (size_t)S.n[i] * S.k[i] / 2, hipMemcpyHostToDevice, cs);
+    if (e != hipSuccess) return e;
+    e = hipMemcpyAsync(const_cast<uint16_t*>(b[i]->scales), a[i]->scales,
+                       (size_t)S.n[i] * (S.k[i] / kGroup) * 2, hipMemcpyHostToDevice, cs);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// true for page-locked host memory (hipHostMalloc), which the copy engines
+// read asynchronously
+bool pinned_host(const void* p) {
+  hipPointerAttribute_t at;
+  if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+    (void)hipGetLastError();  // pageable memory reports an error; clear it
+    return false;
+  }
+  return at.type == hipMemoryTypeHost;
+}
+
 }  // namespace
 
 extern "C" {
@@ -269,102 +445,17 @@ int qlayer_stack_forward_attn(const ql_layer* layers, int32_t n_layers, float* h
                               int64_t d, int64_t d_ff, int32_t group, float eps,
                               const ql_attention_cfg* attn, void* workspace, size_t ws_bytes,
                               void* const* events, ql_stream_t stream) {
-  if (!layers || !h || n_layers < 0) return QL_ERR_ARG;
-  int rc = check_shape(M, d, d, group);
+  if (!layers || n_layers < 0) return QL_ERR_ARG;
+  StackRun r;
+  int rc = stack_setup(h, M, d, d_ff, group, eps, attn, workspace, ws_bytes, events,
+                       (hipStream_t)stream, &r);
   if (rc) return rc;
-  rc = check_shape(M, d_ff, d_ff, group);
-  if (rc) return rc;
-  const bool use_attn = attn && attn->heads != 0;
-  if (use_attn) {
-    rc = check_attention(M, d, attn->heads, attn->seq_len, attn->window, attn->cu_seqlens,
-                         attn->n_seqs);
+  for (int l = 0; l < n_layers; ++l) {
+    rc = check_layer(layers[l]);
     if (rc) return rc;
   }
-  if (!aligned16(h)) return QL_ERR_ALIGN;
-  const StackLayout L = stack_layout(M, d, d_ff);
-  if (!workspace || ws_bytes < L.total) return QL_ERR_WORKSPACE;
-  if (!aligned256(workspace)) return QL_ERR_ALIGN;
-  for (int l = 0; l < n_layers; ++l) {
-    const ql_qmat* mats[4] = {&layers[l].qkv, &layers[l].out, &layers[l].up, &layers[l].down};
-    for (const ql_qmat* q : mats) {
-      if (!q->qweight || !q->scales) return QL_ERR_ARG;
-      if (!aligned16(q->qweight) || ((uintptr_t)q->scales & 1u)) return QL_ERR_ALIGN;
-    }
-  }
-  hipStream_t s = (hipStream_t)stream;
-  char* ws = static_cast<char*>(workspace);
-  uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
-  uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + L.qkv);
-  uint16_t* u = reinterpret_cast<uint16_t*>(ws + L.u);
-  uint16_t* av = reinterpret_cast<uint16_t*>(ws + L.av);
-  float* ns0 = reinterpret_cast<float*>(ws + L.ns0);
-  float* ns1 = reinterpret_cast<float*>(ws + L.ns1);
-  const int64_t Mp = padded_rows(M);
-  const bool small = L.small;
-  hipError_t e = hipSuccess;
-#define QL_TRY(call)               \
-  do {                             \
-    e = (call);                    \
-    if (e != hipSuccess) return QL_ERR_HIP; \
-  } while (0)
-  // optional timing hook: events[8l + 2j] / [8l + 2j + 1] bracket projection j
-  auto mark = [&](int l, int j, int end) -> hipError_t {
-    if (!events) return hipSuccess;
-    void* ev = events[8 * l + 2 * j + end];
-    return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), s) : hipSuccess;
-  };
-  for (int l = 0; l < n_layers; ++l) {
-    const ql_layer& Ly = layers[l];
-    if (small) {
-      QL_TRY(launch_rmsnorm(h, a, nullptr, M, d, 0, eps, false, s));
-      QL_TRY(mark(l, 0, 0));
-      QL_TRY(launch_gemv(a, d, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s));
-      QL_TRY(mark(l, 0, 1));
-      const uint16_t* v = qkv + 2 * d;
-      int64_t ldv = 3 * d;
-      if (use_attn) {
-        QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
-                                attn->window, attn->cu_seqlens, attn->n_seqs, s));
-        v = u;
-        ldv = d;
-      }
-      QL_TRY(mark(l, 1, 0));
-      QL_TRY(launch_gemv(v, ldv, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
-      QL_TRY(mark(l, 1, 1));
-      QL_TRY(launch_rmsnorm(h, a, nullptr, M, d, 0, eps, false, s));
-      QL_TRY(mark(l, 2, 0));
-      QL_TRY(launch_gemv(a, d, Ly.up.qweight, Ly.up.scales, u, d_ff, M, d_ff, d, 1, s));
-      QL_TRY(mark(l, 2, 1));
-      QL_TRY(mark(l, 3, 0));
-      QL_TRY(launch_gemv(u, d_ff, Ly.down.qweight, Ly.down.scales, h, d, M, d, d_ff, 2, s));
-      QL_TRY(mark(l, 3, 1));
-    } else {
-      const GemmPrep vprep{av, d, ns1, 2 * d};   // V slice -> out-projection operand
-      const GemmPrep uprep{u, d_ff, ns1, 0};     // GELU output -> down-projection operand
-      QL_TRY(launch_rmsnorm(h, a, ns0, M, d, Mp, eps, true, s));
-      QL_TRY(mark(l, 0, 0));
-      QL_TRY(launch_gemm(a, ns0, Mp, Ly.qkv.qweight, Ly.qkv.scales, qkv, 3 * d, M, 3 * d, d, 0, s,
-                         use_attn ? nullptr : &vprep));
-      QL_TRY(mark(l, 0, 1));
-      if (use_attn) {
-        QL_TRY(launch_attention(qkv, 3 * d, u, d, M, (int)d, attn->heads, attn->seq_len,
-                                attn->window, attn->cu_seqlens, attn->n_seqs, s));
-        QL_TRY(launch_prep(u, d, av, ns1, M, d, Mp, s));
-      }
-      QL_TRY(mark(l, 1, 0));
-      QL_TRY(launch_gemm(av, ns1, Mp, Ly.out.qweight, Ly.out.scales, h, d, M, d, d, 2, s));
-      QL_TRY(mark(l, 1, 1));
-      QL_TRY(launch_rmsnorm(h, a, ns0, M, d, Mp, eps, true, s));
-      QL_TRY(mark(l, 2, 0));
-      QL_TRY(launch_gemm(a, ns0, Mp, Ly.up.qweight, Ly.up.scales, nullptr, d_ff, M, d_ff, d, 1, s,
-                         &uprep));
-      QL_TRY(mark(l, 2, 1));
-      QL_TRY(mark(l, 3, 0));
-      QL_TRY(launch_gemm(u, ns1, Mp, Ly.down.qweight, Ly.down.scales, h, d, M, d, d_ff, 2, s));
-      QL_TRY(mark(l, 3, 1));
-    }
-  }
-#undef QL_TRY
+  for (int l = 0; l < n_layers; ++l)
+    if (run_block(r, layers[l], l) != hipSuccess) return QL_ERR_HIP;
   return QL_OK;
 }
 
@@ -380,6 +471,71 @@ int qlayer_stack_forward(const ql_layer* layers, int32_t n_layers, float* h, int
                          size_t ws_bytes, ql_stream_t stream) {
   return qlayer_stack_forward_attn(layers, n_layers, h, M, d, d_ff, group, eps, nullptr,
                                    workspace, ws_bytes, nullptr, stream);
+}
+
+size_t qlayer_stack_slot_bytes(int64_t d, int64_t d_ff, int32_t group) {
+  if (check_shape(1, d, d, group) || check_shape(1, d_ff, d_ff, group)) return 0;
+  return slot_layout(d, d_ff).total;
+}
+
+int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers, float* h,
+                                  int64_t M, int64_t d, int64_t d_ff, int32_t group, float eps,
+                                  const ql_attention_cfg* attn, void* workspace, size_t ws_bytes,
+                                  void* slots, size_t slot_bytes, ql_stream_t stream,
+                                  ql_stream_t copy_stream) {
+  if (!host_layers || n_layers < 0 || !slots) return QL_ERR_ARG;
+  if (copy_stream == stream) return QL_ERR_ARG;
+  StackRun r;
+  int rc = stack_setup(h, M, d, d_ff, group, eps, attn, workspace, ws_bytes, nullptr,
+                       (hipStream_t)stream, &r);
+  if (rc) return rc;
+  const SlotLayout S = slot_layout(d, d_ff);
+  if (slot_bytes < 2 * S.total) return QL_ERR_WORKSPACE;
+  if (!aligned256(slots)) return QL_ERR_ALIGN;
+  for (int l = 0; l < n_layers; ++l) {
+    const ql_qmat* mats[4] = {&host_layers[l].qkv, &host_layers[l].out, &host_layers[l].up,
+                              &host_layers[l].down};
+    for (const ql_qmat* q : mats) {
+      if (!q->qweight || !q->scales) return QL_ERR_ARG;
+      if (!pinned_host(q->qweight) || !pinned_host(q->scales)) return QL_ERR_ARG;
+    }
+  }
+  if (n_layers == 0) return QL_OK;
+  hipStream_t s = (hipStream_t)stream, cs = (hipStream_t)copy_stream;
+  // slot k's weights as a device-side layer
+  ql_layer dev[2];
+  for (int k = 0; k < 2; ++k) dev[k] = slot_layer(static_cast<char*>(slots) + k * S.total, S);
+  // copied[k]: slot k holds the layer the next block reads; freed[k]: the
+  // block that last read slot k has finished
+  hipEvent_t copied[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
+  int out = QL_OK;
+  for (int k = 0; k < 2 && out == QL_OK; ++k)
+    if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&freed[k], hipEventDisableTiming) != hipSuccess)
+      out = QL_ERR_HIP;
+  auto copy_layer = [&](int l, int k) -> hipError_t {
+    hipError_t e = copy_matrices(host_layers[l], dev[k], d, d_ff, cs);
+    return e != hipSuccess ? e : hipEventRecord(copied[k], cs);
+  };
+  if (out == QL_OK && copy_layer(0, 0) != hipSuccess) out = QL_ERR_HIP;
+  for (int l = 0; l < n_layers && out == QL_OK; ++l) {
+    const int k = l & 1, nk = k ^ 1;
+    if (l + 1 < n_layers) {
+      // the next layer goes into the other slot once block l - 1 is done with it
+      if (l >= 1 && hipStreamWaitEvent(cs, freed[nk], 0) != hipSuccess) { out = QL_ERR_HIP; break; }
+      if (copy_layer(l + 1, nk) != hipSuccess) { out = QL_ERR_HIP; break; }
+    }
+    if (hipStreamWaitEvent(s, copied[k], 0) != hipSuccess) { out = QL_ERR_HIP; break; }
+    if (run_block(r, dev[k], l) != hipSuccess) { out = QL_ERR_HIP; break; }
+    if (hipEventRecord(freed[k], s) != hipSuccess) { out = QL_ERR_HIP; break; }
+  }
+  // events may be destroyed while work that records them is still queued:
+  // the runtime releases them once they complete
+  for (int k = 0; k < 2; ++k) {
+    if (copied[k]) (void)hipEventDestroy(copied[k]);
+    if (freed[k]) (void)hipEventDestroy(freed[k]);
+  }
+  return out;
 }
 
 void qlinear_release(void) {

@@ -32,7 +32,8 @@ def test_header_declares_the_boundary():
                  "qlinear_forward_ex", "qlinear_workspace_bytes", "qlinear_status_string",
                  "qlayer_stack_workspace_bytes", "qlinear_rmsnorm", "qlinear_release",
                  "qlayer_stack_workspace_offsets", "qlinear_attention",
-                 "qlayer_stack_forward_attn", "qlinear_attention_varlen"]:
+                 "qlayer_stack_forward_attn", "qlinear_attention_varlen",
+                 "qlayer_stack_forward_streamed", "qlayer_stack_slot_bytes"]:
         assert need in names, need
 
 
@@ -150,3 +151,29 @@ def test_attention_varlen_errors_without_launch(lib):
     assert f(q, 768, o, 256, 100, 256, 2, cu, 3, 0, 8, None) == 1        # max length 0
     assert f(q, 768, o, 256, 100, 256, 2, ctypes.c_void_p((1 << 12) + 2), 3, 64, 8, None) == 3
     assert f(q, 768, o, 256, 100, 384, 2, cu, 3, 64, 8, None) == 2       # head dim 192
+
+
+def test_streamed_stack_errors_without_launch(lib):
+    f = lib.qlayer_stack_forward_streamed
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i32, vp, i64, i64, i64, i32, ctypes.c_float, vp, vp, sz, vp, sz, vp, vp]
+    f.restype = ctypes.c_int
+    sb = lib.qlayer_stack_slot_bytes
+    sb.argtypes = [i64, i64, i32]
+    sb.restype = sz
+    slot = sb(256, 1024, 128)
+    # codes + scales of qkv, out, up, down, each 256-byte aligned
+    assert slot == (3 * 256 * 128 + 3 * 256 * 2 * 2 + 256 * 128 + 256 * 2 * 2 +
+                    1024 * 128 + 1024 * 2 * 2 + 256 * 512 + 256 * 8 * 2)
+    assert sb(256, 1000, 128) == 0
+    p, s1, s2 = ctypes.c_void_p(4096), ctypes.c_void_p(1 << 12), ctypes.c_void_p(1 << 13)
+    big = 1 << 30
+    # the copy stream must differ from the compute stream
+    assert f(p, 1, p, 8, 256, 1024, 128, 1e-5, None, p, big, p, big, s1, s1) == 1
+    # no slots
+    assert f(p, 1, p, 8, 256, 1024, 128, 1e-5, None, p, big, None, big, s1, s2) == 1
+    # slots smaller than two blocks
+    assert f(p, 1, p, 8, 256, 1024, 128, 1e-5, None, p, big, p, 2 * slot - 1, s1, s2) == 6
+    # slots not 256-byte aligned
+    assert f(p, 1, p, 8, 256, 1024, 128, 1e-5, None, p, big, ctypes.c_void_p(4096 + 16), big,
+             s1, s2) == 3
