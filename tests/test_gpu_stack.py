@@ -114,17 +114,30 @@ def test_zero_scales_keep_residual_full_96_layers(ql):
     assert torch.equal(h.cpu(), torch.from_numpy(h0))
 
 
-def test_full_width_block_sampled_tokens(ql):
-    """One 175B-width block at M = 4096: 8 sampled tokens against the oracle."""
+def test_full_width_two_blocks_sampled_tokens(ql):
+    """Two 175B-width blocks (layers 0 and 1 of the seeded stack) at
+    M = 4096: 16 sampled tokens against the oracle run through both blocks
+    from the same seeded input (tokens never mix in this stack, so the
+    oracle's rows are exact), checked after each block."""
     d, dff, M = 12288, 49152, 4096
-    say("stack full-width block")
-    layer = _packed_layer_direct(synth.SEED_STACK, 0, d, dff)
+    say("stack full-width blocks 0 and 1")
+    layers = [_packed_layer_direct(synth.SEED_STACK, l, d, dff) for l in range(2)]
+    dev_layers = [_to_dev(x) for x in layers]
     h0 = synth.residual_f32(synth.SEED_STACK, M, d)
-    h, _ = _run(ql, [_to_dev(layer)], h0, dff)
-    rows = np.sort(np.random.default_rng(8).choice(M, 8, replace=False))
-    got = h.cpu().numpy()[rows].astype(np.float64)
-    say("  oracle on sampled tokens")
-    ref = O.stack_layer(h0[rows], layer).astype(np.float64)
-    err = O.rel_fro(got - h0[rows], ref - h0[rows])
-    say(f"  rel err of the residual update: {err:.3e}")
-    assert err <= 5e-3
+    rows = np.sort(np.random.default_rng(8).choice(M, 16, replace=False))
+    h1, _ = _run(ql, dev_layers[:1], h0, dff)
+    got1 = h1.cpu().numpy()[rows].astype(np.float64)
+    del h1
+    h2, _ = _run(ql, dev_layers, h0, dff)
+    got2 = h2.cpu().numpy()[rows].astype(np.float64)
+    del h2, dev_layers
+    say("  oracle on sampled tokens, block 0")
+    ref1 = O.stack_layer(h0[rows], layers[0])
+    err1 = O.rel_fro(got1 - h0[rows], ref1.astype(np.float64) - h0[rows])
+    say(f"  block 0: rel err of the residual update {err1:.3e}")
+    assert err1 <= 5e-3
+    say("  oracle on sampled tokens, block 1")
+    ref2 = O.stack_layer(ref1, layers[1]).astype(np.float64)
+    err2 = O.rel_fro(got2 - h0[rows], ref2 - h0[rows])
+    say(f"  blocks 0-1: rel err of the residual update {err2:.3e}")
+    assert err2 <= 5e-3
