@@ -5,15 +5,17 @@
 // sequence with i - window < j <= i.  Head dimension 128.
 //
 // One workgroup (8 waves) owns 128 queries of one head; wave w owns 16 of
-// them.  Key blocks of 64 are staged in LDS (K row-major, V transposed), the
-// next block's loads in flight while the current one is computed.  The
-// scores are computed transposed, S^T = K Q^T (16x16x32 bf16 MFMAs with K as
-// the row operand), so that a lane ends up holding, for its query, exactly
-// the keys it feeds as the column operand of O^T += V^T P^T: nothing moves
-// between the two products.  Softmax is online in fp32 (base 2); P is
-// rounded to bf16 for the second product and the row sums add the rounded
-// values, so the weights the product sees sum to one; O stays fp32 until the
-// final bf16 store.
+// them.  Key blocks of 64 keys go global -> LDS by direct-to-LDS copies into a
+// two-stage ring (K and V both row-major, swizzled), the next block's copies
+// in flight while the current one is computed.  The scores are computed
+// transposed, S^T = K Q^T (16x16x32 bf16 MFMAs with K as the row operand), so
+// that a lane ends up holding, for its query, exactly the keys it feeds as
+// the column operand of O^T += V^T P^T: nothing moves between the two
+// products.  The V^T operand is read from the row-major V tile with the
+// transposing LDS read (ds_read_b64_tr_b16).  Softmax is online in fp32 (base
+// 2); P is rounded to bf16 for the second product and the row sums add the
+// rounded values, so the weights the product sees sum to one; O stays fp32
+// until the final bf16 store.
 #include <algorithm>
 
 #include "ql_device.h"
@@ -45,18 +47,10 @@ __device__ __forceinline__ int k_msk(int r) {
   r &= 15;
   return r ^ ((((r >> 2) ^ (r >> 3)) & 1) << 2);
 }
-// V^T tile: dim row e holds the block's 64 keys (128 bytes) in the order
-// vpos(key); chunk c of row e sits at slot e * 8 + (c ^ v_msk(e)).
-__device__ __forceinline__ int v_msk(int e) {
-  return (((e >> 1) & 1) | (((e >> 3) & 1) << 1)) << 1;
-}
-// key = 32 t + 16 f + 4 hh + r  ->  32 t + 8 hh + 4 f + r: the 8 keys that lane
-// group hh feeds to one V^T P^T step (fragments 2t and 2t+1 of S^T) are then
-// one contiguous chunk, 4t + hh.
-__device__ __forceinline__ int vpos(int key) {
-  const int t = key >> 5, f = (key >> 4) & 1, hh = (key >> 2) & 3, r = key & 3;
-  return 32 * t + 8 * hh + 4 * f + r;
-}
+// V tile: key r keeps its 16-byte chunk c (dims 8c .. 8c+7) at slot
+// r * 16 + (c ^ v_swz(r)).  A transposing read covers 8 keys x 32 bytes per
+// half-wave; the swizzle puts those 8 rows' 32-byte pieces in distinct banks.
+__device__ __forceinline__ int v_swz(int r) { return (r & 7) << 1; }
 
 // Reductions over the 4 lanes of a query (lanes lr, lr + 16, lr + 32,
 // lr + 48).  v_permlane16_swap with both operands equal to v leaves, in each
@@ -84,58 +78,79 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{a, b}), bf16x2));
 }
 
-// The next key block's K and V, staged in registers while the current block
-// is computed.  Thread t holds K chunks t and t + 512 of the 64 x 128 tile
-// and V chunk (t >> 5) of keys 2 (t & 31) and 2 (t & 31) + 1.
-struct Staged {
-  u32x4 k[2];
-  u32x4 v[2];
-};
+// One 16-byte direct-to-LDS copy: lane l writes lds + 16 l.  Inline assembly
+// so that the compiler does not track it (it would otherwise wait for the
+// copy right after issuing it); the kernel waits with an explicit
+// s_waitcnt.  M0 carries the LDS base and is saved and restored (the
+// compiler reserves it); one wait state separates its write from the load.
+__device__ __forceinline__ void copy16_to_lds(const void* src, const void* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(lds));
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %[sv], m0\n\t"
+      "s_mov_b32 m0, %[l]\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %[a], off\n\t"
+      "s_mov_b32 m0, %[sv]"
+      : [sv] "=&s"(saved)
+      : [a] "v"(src), [l] "s"(l)
+      : "memory");
+}
 
-__device__ __forceinline__ void load_block(const AttnParams& p, int64_t seq0, int L, int j0,
-                                           int tid, int64_t kcol, int64_t vcol, Staged& st) {
-  // keys past the sequence end (last block of a ragged sequence) repeat its
-  // last row; causality masks them for every real query
+// Copies of key block j0 into one stage: wave w issues copies i = 0, 1 of K
+// and of V, copy i covering the 16-byte slots (8 i + w) * 64 + lane, i.e.
+// keys 4 (8 i + w) .. +3.  src[i] is the lane's source for key block 0
+// (sequence row key, its swizzled chunk of K; V follows at +d elements);
+// whole blocks advance it by j0 rows.  In the last block of a ragged
+// sequence, keys past its end repeat its last row; causality masks them for
+// every real query.
+__device__ __forceinline__ void issue_block(const AttnParams& p, const uint16_t* const (&src)[2][2],
+                                            int L, int j0, int wave, u32x4* sK, u32x4* sV) {
+  const int64_t adv = (int64_t)j0 * p.ldq;
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int c = k * kThreads + tid, key = c >> 4, ch = c & 15;
-    const int64_t row = seq0 + min(j0 + key, L - 1);
-    st.k[k] = *reinterpret_cast<const u32x4*>(p.qkv + row * p.ldq + kcol + ch * 8);
-  }
-  const int a2 = tid & 31, ch = tid >> 5;
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int64_t row = seq0 + min(j0 + 2 * a2 + r, L - 1);
-    st.v[r] = *reinterpret_cast<const u32x4*>(p.qkv + row * p.ldq + vcol + ch * 8);
+  for (int i = 0; i < 2; ++i) {
+    const int key0 = (i * 8 + wave) * 4;  // first key of the copy (wave-uniform)
+    const uint16_t* ks = src[i][0] + adv;
+    const uint16_t* vs = src[i][1] + adv;
+    if (j0 + key0 + 3 >= L) {  // rare: the copy reaches past the sequence end
+      const int key = key0 + ((int)(threadIdx.x & 63) >> 4);
+      const int64_t back = (int64_t)(min(j0 + key, L - 1) - (j0 + key)) * p.ldq;
+      ks += back;
+      vs += back;
+    }
+    copy16_to_lds(ks, sK + (i * 8 + wave) * 64);
+    copy16_to_lds(vs, sV + (i * 8 + wave) * 64);
   }
 }
 
-// K row-major (swizzled); V transposed: per dim, the two keys' values as one
-// dword at their (adjacent) vpos positions.  Odd chunks write their dims in
-// the order e ^ 1, so that a wave's 64 dwords fall in 64 distinct banks.
-__device__ __forceinline__ void store_block(const Staged& st, int tid, u32x4* sK, uint32_t* sV1) {
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int c = k * kThreads + tid, key = c >> 4, ch = c & 15;
-    sK[key * 16 + (ch ^ k_msk(key))] = st.k[k];
-  }
-  const int a2 = tid & 31, ch = tid >> 5, odd = ch & 1;
-  const int pk = vpos(2 * a2), pc = pk >> 3, q = (pk & 7) >> 1;
-  // dim 8 ch + e' sits in half e' & 1 of dword e' >> 1 of both rows; with
-  // e' = e ^ odd only the half (the byte selector) depends on the thread
-  const uint32_t sel_lo = odd ? 0x07060302u : 0x05040100u;
-  const uint32_t sel_hi = odd ? 0x05040100u : 0x07060302u;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int dim = ch * 8 + (e ^ odd);
-    sV1[(dim * 8 + (pc ^ v_msk(dim))) * 4 + q] =
-        __builtin_amdgcn_perm(st.v[1][e >> 1], st.v[0][e >> 1], (e & 1) ? sel_hi : sel_lo);
-  }
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// V^T operand of one 32-key step for dims 16 df .. 16 df + 15: lane (lr, h)
+// gets V[32 t2 + 16 f + 4 h + j][16 df + lr] as element 4 f + j.  In a
+// transposing read, lane i = 4a + b of a 16-lane group receives element b of
+// the 8-byte pieces addressed by lanes a, a + 4, a + 8, a + 12; so lane
+// (lr, h) addresses key 32 t2 + 16 f + 4 h + lr / 4, dims 16 df + 4 (lr % 4)
+// .. + 3.  With the V swizzle that is byte
+//   (32 t2 + 16 f) * 256 + vt_lane(df, h, lr)
+// of the stage: the (t2, f) part is a constant offset of the read.
+__device__ __forceinline__ uint32_t vt_lane(int df, int h, int lr) {
+  const int key = 4 * h + (lr >> 2);  // (mod 8 the same for every t2, f)
+  const int chunk = 2 * df + ((lr >> 1) & 1);
+  return (uint32_t)(key * 256 + ((chunk ^ v_swz(key)) << 4) + ((lr & 1) << 3));
+}
+template <int T2>
+__device__ __forceinline__ bf16x8 load_vt(uint32_t addr) {
+  const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      reinterpret_cast<lds_bf16x4*>((uintptr_t)(addr + T2 * 32 * 256)));
+  const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      reinterpret_cast<lds_bf16x4*>((uintptr_t)(addr + T2 * 32 * 256 + 16 * 256)));
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
 
 __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
-  __shared__ u32x4 sK[kBK * 16];  // 16 KB
-  __shared__ u32x4 sV[kDh * 8];   // 16 KB
+  __shared__ u32x4 sK[2][kBK * 16];  // two stages of 16 KB
+  __shared__ u32x4 sV[2][kBK * 16];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 4, lr = lane & 15;
@@ -192,15 +207,30 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
 
   const int ilast = min(i0 + kBQ, L) - 1;  // last real query of the workgroup
   const int kb_lo = max(0, i0 - p.W + 1) / kBK, kb_hi = ilast / kBK;
-  uint32_t* sV1 = reinterpret_cast<uint32_t*>(sV);
-  Staged st;
-  load_block(p, seq0, L, kb_lo * kBK, tid, kcol, vcol, st);
+  const uint16_t* src[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int slot = (i * 8 + wave) * 64 + lane, key = slot >> 4, ps = slot & 15;
+    const uint16_t* row = p.qkv + (seq0 + key) * p.ldq;
+    src[i][0] = row + kcol + (ps ^ k_msk(key)) * 8;
+    src[i][1] = row + vcol + (ps ^ v_swz(key)) * 8;
+  }
+  uint32_t vt_addr[8];  // LDS byte address of this lane's V^T reads in stage 0, per df
+#pragma unroll
+  for (int df = 0; df < 8; ++df)
+    vt_addr[df] = (uint32_t)reinterpret_cast<uintptr_t>(sV[0]) + vt_lane(df, h, lr);
+  issue_block(p, src, L, kb_lo * kBK, wave, sK[kb_lo & 1], sV[kb_lo & 1]);
   for (int kb = kb_lo; kb <= kb_hi; ++kb) {
     const int j0 = kb * kBK;
-    __syncthreads();  // the previous block's reads are done
-    store_block(st, tid, sK, sV1);
+    const u32x4* cK = sK[kb & 1];
+    const uint32_t vstage = (kb & 1) * (uint32_t)sizeof(sV[0]);  // byte offset of the stage
+    // this wave's copies of block kb have landed (they are its only vector
+    // memory operations in flight); after the barrier every wave's copies
+    // are visible and every read of the other stage (block kb - 1) is done
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (kb < kb_hi) load_block(p, seq0, L, j0 + kBK, tid, kcol, vcol, st);
+    if (kb < kb_hi)
+      issue_block(p, src, L, j0 + kBK, wave, sK[(kb + 1) & 1], sV[(kb + 1) & 1]);
 
     // skip blocks no query of this wave can see (wave-uniform)
     if (qw0 >= L || j0 > qw1 || qw0 - (j0 + kBK - 1) >= p.W) continue;
@@ -214,7 +244,7 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
       f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        c = mfma16x16x32(as_bf16x8(sK[key * 16 + ((h * 4 + s) ^ k_msk(key))]), qf[s], c);
+        c = mfma16x16x32(as_bf16x8(cK[key * 16 + ((h * 4 + s) ^ k_msk(key))]), qf[s], c);
       sc[kf] = c;
     }
     if (!full) {
@@ -271,10 +301,8 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
     }
 #pragma unroll
     for (int df = 0; df < 8; ++df) {
-      const int dim = df * 16 + lr;
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2)
-        o[df] = mfma16x16x32(as_bf16x8(sV[dim * 8 + ((4 * t2 + h) ^ v_msk(dim))]), pb[t2], o[df]);
+      o[df] = mfma16x16x32(load_vt<0>(vt_addr[df] + vstage), pb[0], o[df]);
+      o[df] = mfma16x16x32(load_vt<1>(vt_addr[df] + vstage), pb[1], o[df]);
     }
   }
 
