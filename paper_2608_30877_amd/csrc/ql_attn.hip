@@ -5,7 +5,8 @@
 // sequence with i - window < j <= i.  Head dimension 128.
 //
 // One workgroup (8 waves) owns 128 queries of one head; wave w owns 16 of
-// them.  Key blocks of 64 keys go global -> LDS by direct-to-LDS copies into a
+// them.  (16 waves x 256 queries halve the key / value copies but measure
+// slower: one workgroup per CU, and 16 waves meet at every barrier.)  Key blocks of 64 keys go global -> LDS by direct-to-LDS copies into a
 // two-stage ring (K and V both row-major, swizzled), the next block's copies
 // in flight while the current one is computed.  The scores are computed
 // transposed, S^T = K Q^T (16x16x32 bf16 MFMAs with K as the row operand), so
@@ -26,9 +27,12 @@ namespace ql {
 namespace {
 
 constexpr int kDh = 128;  // head dimension
-constexpr int kBQ = 128;  // queries per workgroup (8 waves x 16)
-constexpr int kThreads = 512;
+constexpr int kWaves = 8;                // waves per workgroup, 16 queries each
+constexpr int kThreads = kWaves * 64;
+constexpr int kBQ = kWaves * 16;         // queries per workgroup
 constexpr int kBK = 64;   // keys per LDS block
+constexpr int kCopies = kBK * 16 / 64 / kWaves;  // 16-byte copies of K (and of V) per wave per block
+static_assert(kCopies >= 1 && kCopies * kWaves * 64 == kBK * 16, "copies cover the tile");
 
 struct AttnParams {
   const uint16_t* qkv;
@@ -97,19 +101,20 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, const void* lds) 
       : "memory");
 }
 
-// Copies of key block j0 into one stage: wave w issues copies i = 0, 1 of K
-// and of V, copy i covering the 16-byte slots (8 i + w) * 64 + lane, i.e.
-// keys 4 (8 i + w) .. +3.  src[i] is the lane's source for key block 0
+// Copies of key block j0 into one stage: wave w issues copies i < kCopies of
+// K and of V, copy i covering the 16-byte slots (kWaves i + w) * 64 + lane,
+// i.e. keys 4 (kWaves i + w) .. +3.  src[i] is the lane's source for key block 0
 // (sequence row key, its swizzled chunk of K; V follows at +d elements);
 // whole blocks advance it by j0 rows.  In the last block of a ragged
 // sequence, keys past its end repeat its last row; causality masks them for
 // every real query.
-__device__ __forceinline__ void issue_block(const AttnParams& p, const uint16_t* const (&src)[2][2],
+__device__ __forceinline__ void issue_block(const AttnParams& p,
+                                            const uint16_t* const (&src)[kCopies][2],
                                             int L, int j0, int wave, u32x4* sK, u32x4* sV) {
   const int64_t adv = (int64_t)j0 * p.ldq;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int key0 = (i * 8 + wave) * 4;  // first key of the copy (wave-uniform)
+  for (int i = 0; i < kCopies; ++i) {
+    const int key0 = (i * kWaves + wave) * 4;  // first key of the copy (wave-uniform)
     const uint16_t* ks = src[i][0] + adv;
     const uint16_t* vs = src[i][1] + adv;
     if (j0 + key0 + 3 >= L) {  // rare: the copy reaches past the sequence end
@@ -118,8 +123,8 @@ __device__ __forceinline__ void issue_block(const AttnParams& p, const uint16_t*
       ks += back;
       vs += back;
     }
-    copy16_to_lds(ks, sK + (i * 8 + wave) * 64);
-    copy16_to_lds(vs, sV + (i * 8 + wave) * 64);
+    copy16_to_lds(ks, sK + (i * kWaves + wave) * 64);
+    copy16_to_lds(vs, sV + (i * kWaves + wave) * 64);
   }
 }
 
@@ -207,10 +212,10 @@ __global__ __launch_bounds__(kThreads, 4) void k_attn(AttnParams p) {
 
   const int ilast = min(i0 + kBQ, L) - 1;  // last real query of the workgroup
   const int kb_lo = max(0, i0 - p.W + 1) / kBK, kb_hi = ilast / kBK;
-  const uint16_t* src[2][2];
+  const uint16_t* src[kCopies][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int slot = (i * 8 + wave) * 64 + lane, key = slot >> 4, ps = slot & 15;
+  for (int i = 0; i < kCopies; ++i) {
+    const int slot = (i * kWaves + wave) * 64 + lane, key = slot >> 4, ps = slot & 15;
     const uint16_t* row = p.qkv + (seq0 + key) * p.ldq;
     src[i][0] = row + kcol + (ps ^ k_msk(key)) * 8;
     src[i][1] = row + vcol + (ps ^ v_swz(key)) * 8;
