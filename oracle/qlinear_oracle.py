@@ -44,7 +44,8 @@ __all__ = [
     "GROUP", "QMAX", "QMIN", "ERR_RANGE", "OracleRangeError",
     "bf16_bits_to_f64", "f64_to_bf16_bits", "f16_bits_to_f32",
     "quantize_pack", "unpack_codes", "dequant", "qlinear_ref",
-    "qlinear_ref_cols", "gelu", "rmsnorm_bf16", "attention_ref", "stack_layer",
+    "qlinear_ref_cols", "gelu", "rmsnorm_bf16", "attention_ref", "attention_rows_ref",
+    "stack_layer",
     "rel_fro",
 ]
 
@@ -274,6 +275,33 @@ def attention_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len, window: int
             e = np.exp(s - s.max(axis=1, keepdims=True))
             out[rows, c] = (e / e.sum(axis=1, keepdims=True)) @ v
         p0 += L
+    return out
+
+
+def attention_rows_ref(qkv_bits: np.ndarray, d: int, heads: int, seq_len: int, window: int,
+                       rows) -> np.ndarray:
+    """attention_ref's output for the given token rows only (uniform
+    sequences of seq_len tokens): the same definition, evaluated for the
+    selected queries against the keys each may see, so that long sequences
+    (a 32K window) can be checked without the seq_len x seq_len score
+    matrix.  Returns [len(rows), d] (fp64)."""
+    x = bf16_bits_to_f64(np.asarray(qkv_bits))
+    dh = d // heads
+    if d % heads or x.shape[0] % seq_len:
+        raise ValueError("d must split into heads and M into whole sequences")
+    out = np.empty((len(rows), d), dtype=np.float64)
+    for n, t in enumerate(rows):
+        p0 = (t // seq_len) * seq_len
+        i = t - p0
+        lo = p0 + max(0, i - window + 1)
+        for hh in range(heads):
+            c = slice(hh * dh, (hh + 1) * dh)
+            q = x[t, c]
+            k = x[lo:t + 1, d + hh * dh:d + (hh + 1) * dh]
+            v = x[lo:t + 1, 2 * d + hh * dh:2 * d + (hh + 1) * dh]
+            s = (k @ q) / np.sqrt(dh)
+            e = np.exp(s - s.max())
+            out[n, c] = (e / e.sum()) @ v
     return out
 
 

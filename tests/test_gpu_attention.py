@@ -127,6 +127,27 @@ def test_attention_full_size_sampled_heads(ql):
         say(f"  pair {pair} head {hh}: rel err {err:.3e}")
 
 
+@pytest.mark.parametrize("L,W", [(32768, 32768), (16384, 5000)])
+def test_attention_32k_window_sampled_rows(ql, L, W):
+    """The paper's 32K window used in full: sequences of 32768 (or 16384)
+    tokens, one head; 48 sampled query rows (first, last, window edges and
+    random) against the oracle's row-sampled attention."""
+    M, heads = 32768, 1
+    d = 128 * heads
+    say(f"attention long sequences L={L} W={W}")
+    qkv = synth.qkv_bf16(31 + W, M, d, std=1.0)
+    out = host_u16(ql.attention(dev_u16(qkv), heads, L, W))
+    rng = np.random.default_rng(W)
+    edges = [0, 1, W - 1, W, W + 1, L - 1, L, L + 1, L + W - 1, L + W, M - 1]
+    rows = sorted(set([r for r in edges if 0 <= r < M] + [int(r) for r in rng.choice(M, 39, replace=False)]))
+    ref = O.attention_rows_ref(qkv, d, heads, L, W, rows)
+    got = bf16_as_f64(out[rows])
+    vmax = np.abs(bf16_as_f64(qkv[:, 2 * d:])).max()
+    bad = np.abs(got - ref) > TOL * (vmax + np.abs(ref))
+    assert not bad.any(), f"rows {np.array(rows)[bad.any(axis=1)]}"
+    assert O.rel_fro(got, ref) <= 5e-3
+
+
 def test_attention_argument_errors(ql):
     qkv = torch.zeros((128, 3 * 256), dtype=torch.int16, device="cuda")
     with pytest.raises(ql.QLError) as e:

@@ -465,3 +465,17 @@ def test_stack_layer_with_width_one_attention_matches_stand_in():
     layer = {"qkv": mk(0, 3 * d, d), "out": mk(1, d, d), "up": mk(2, dff, d), "down": mk(3, d, dff)}
     h = synth.residual_f32(9, M, d)
     np.testing.assert_array_equal(O.stack_layer(h, layer), O.stack_layer(h, layer, attn=(1, 3, 1)))
+
+
+def test_attention_rows_match_the_full_attention():
+    """The row-sampled form agrees with attention_ref on every row (windows
+    shorter and longer than the sequence), to rounding of the fp64 sums."""
+    rng = np.random.default_rng(17)
+    d, heads, L = 16, 2, 9
+    M = 3 * L
+    bits = _qkv(*[rng.standard_normal((M, d)) * 2 for _ in range(3)])
+    for window in (1, 4, 9, 50):
+        full = O.attention_ref(bits, d, heads, L, window)
+        rows = list(range(M))
+        got = O.attention_rows_ref(bits, d, heads, L, window, rows)
+        np.testing.assert_allclose(got, full, rtol=1e-12, atol=1e-12)
