@@ -180,9 +180,12 @@ def bench_stack(args, ql, synth, torch):
     if not args.no_attention:
         out["with_attention"] = bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d,
                                                       dff, pairs)
-        out["ragged"] = bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M, d, dff)
-        out["ragged"]["vs_padded_with_attention"] = round(
-            out["ragged"]["pairs_per_s"] / out["with_attention"]["pairs_per_s"], 4)
+        if not args.no_ragged:
+            out["ragged"] = bench_stack_ragged(args, ql, synth, torch, arr, h0, ws, L, M, d, dff)
+            out["ragged"]["vs_padded_with_attention"] = round(
+                out["ragged"]["pairs_per_s"] / out["with_attention"]["pairs_per_s"], 4)
+    if not args.no_sweep:
+        out["batch_sweep"] = bench_batch_sweep(ql, synth, torch, arr, L, d, dff)
     if not args.no_streamed:
         out["host_streamed"] = bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d,
                                                     dff, pairs, ms)
@@ -233,6 +236,31 @@ def bench_stack_attention(args, ql, torch, arr, h, h0, ws, L, M, d, dff, pairs):
             "attention_GBps": round(abytes / t_attn / 1e9, 1),
             "attention_frac_hbm_peak": round(abytes / t_attn / 1e9 / PEAK_HBM_GBS, 4),
             "attention_causal_tflops": round(flops / t_attn / 1e12, 1)}
+
+
+def bench_batch_sweep(ql, synth, torch, arr, L, d, dff, pair_counts=(1, 2, 4, 16)):
+    """The same resident stack (width-1 stand-in) at other batch sizes: one
+    warmup and one timed forward per size, pairs of 512 tokens."""
+    res = []
+    for n in pair_counts:
+        M = n * TOKENS_PER_PAIR
+        ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
+        h0 = torch.from_numpy(synth.residual_f32(synth.SEED_STACK + n, M, d)).cuda()
+        h = torch.empty_like(h0)
+        h.copy_(h0)
+        ql.stack_forward(arr, h, dff, ws)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        h.copy_(h0)
+        ql.stack_forward(arr, h, dff, ws)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
+        flops = L * 2 * M * d * (3 * d + d + 2 * dff)
+        res.append({"pairs": n, "tokens": M, "ms_per_step": round(ms, 2),
+                    "pairs_per_s": round(n / (ms / 1e3), 4),
+                    "tflops": round(flops / (ms / 1e3) / 1e12, 1)})
+        del ws, h0, h
+    return res
 
 
 STREAM_POOL = 16   # distinct blocks kept in page-locked host memory for the streamed variant
@@ -481,6 +509,10 @@ def main():
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-attention", action="store_true",
                     help="skip the stack variants with sliding-window attention")
+    ap.add_argument("--no-ragged", action="store_true",
+                    help="skip the ragged-batch variant")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the stack at other batch sizes")
     ap.add_argument("--no-streamed", action="store_true",
                     help="skip the variant with the weights streamed from host memory")
     args = ap.parse_args()
