@@ -220,6 +220,14 @@ template <int EPI, bool PREP, int IF>
 __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int64_t n0, int wave,
                                            int lane, const f32x4 (&acc)[IF][JF], float* part) {
   constexpr int BM = TileM<IF>::BM;
+  if constexpr (PREP) {
+    // a tile left of the prepared columns (the Q and K thirds of a QKV
+    // projection) is stored plainly, without the row sums and their exchange
+    if (n0 + BN <= p.pcol0) {
+      store_tile<EPI, false, IF>(p, m0, n0, wave, lane, acc, part);
+      return;
+    }
+  }
   const int h = lane >> 4, lr = lane & 15;
   float rs[IF][4];
 #pragma unroll
