@@ -517,8 +517,8 @@ def main():
                     help="skip the variant with the weights streamed from host memory")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(data parallelism over pairs would need no exchange; see the design notes)",
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(pairs are independent, so data parallelism over pairs would need no exchange)",
               file=sys.stderr)
         sys.exit(2)
 
