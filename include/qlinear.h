@@ -153,7 +153,8 @@ size_t qlayer_stack_workspace_bytes(int64_t M, int64_t d, int64_t d_ff,
  *     v   = qkv[:, 2d:3d]                    (sliding-window attention of
  *                                             width 1 is the identity on V;
  *                                             the model of Sec. 1 / 2.1 uses
- *                                             sliding-window attention)
+ *                                             sliding-window attention, which
+ *                                             qlayer_stack_forward_attn runs)
  *     h  += v * W_o^T                        (fp32)
  *     a2  = bf16(RMSNorm(h))
  *     u   = bf16(gelu_erf(a2 * W_up^T))
@@ -166,7 +167,9 @@ size_t qlayer_stack_workspace_bytes(int64_t M, int64_t d, int64_t d_ff,
  *              [0]        a / a2 staging  bf16 [M][d]   (internal layout)
  *              [qkv_off]  qkv             bf16 [M][3d]  (row-major)
  *              [u_off]    u               bf16 [M][max(d, d_ff)]: row-major when
- *                         M <= 16; for larger M the MFMA operand layout,
+ *                         M <= 16 (and d, d_ff <= 49152, where every
+ *                         projection runs the small-batch kernel); otherwise
+ *                         the MFMA operand layout,
  *                         in which each 8-element chunk of a row holds
  *                         elements (0,4,1,5,2,6,3,7) of that chunk
  *              then, for M > 16, the prepared V copy and two correction-term
