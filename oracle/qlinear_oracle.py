@@ -27,13 +27,16 @@ this library fixes it, and the functions below are that scheme written out:
 
 The transformer-block steps (RMSNorm, GELU, the attention between the QKV
 and output projections -- either the width-1 sliding-window stand-in or the
-causal sliding-window attention of ``attention_ref`` -- fp32 residual
-stream) are written out in ``rmsnorm_bf16``, ``gelu``, ``attention_ref`` and
-``stack_layer``.
+causal sliding-window attention of ``attention_ref`` over uniform or ragged
+sequences -- fp32 residual stream) are written out in ``rmsnorm_bf16``,
+``gelu``, ``attention_ref`` and ``stack_layer``; ``attention_rows_ref``
+evaluates attention_ref's definition for selected query rows only (long
+sequences).
 
 Every function here is pinned by CPU tests against something other than
 itself: exact rational brute force, closed forms, special cases, library
-routines of a different kind.  None is "parity unpinned".
+routines of a different kind (attention_rows_ref against attention_ref,
+which closed forms pin).  None is "parity unpinned".
 """
 from __future__ import annotations
 
