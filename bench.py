@@ -470,33 +470,52 @@ def bench_prefill(ql, synth, torch, reps=10):
     return res
 
 
-def cpu_baseline(synth, d=12288, dff=49152, tokens=64, layers=96):
-    """The oracle as it stands, on one 175B-width block over `tokens` tokens
-    (packed weights drawn directly by the seeded generator)."""
+def cpu_baseline(synth, d=12288, dff=49152, tokens=4096, layers=96):
+    """The oracle as it stands, timed on the host cores on a bounded sample
+    of the benched workload: one 175B-width projection (the out projection,
+    12288 x 12288) over the full batch of `tokens` tokens.  The oracle's two
+    steps are timed apart: dequantization (oracle.dequant, independent of
+    the batch) and the fp64 product (oracle.qlinear_ref minus its own
+    dequantization).  A block's four projections hold 12x this matrix's
+    weights and, at the same batch, 12x its flops, so both terms scale by
+    12 per block and by `layers` per forward (extrapolated)."""
     import numpy as np
     import oracle as O
 
+    cpu_count = os.cpu_count()
+    affinity = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        limiter = threadpool_limits(limits=affinity)
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        limiter, blas_threads = None, None
 
-    def mk(i, n, k):
-        s = synth.matrix_seed(synth.SEED_STACK + 100, 0, i)
-        return synth.random_packed_bytes(s, n, k), synth.random_scales_f16(s, n, k // 128)
-
-    layer = {"qkv": mk(0, 3 * d, d), "out": mk(1, d, d), "up": mk(2, dff, d),
-             "down": mk(3, d, dff)}
-    h = synth.residual_f32(synth.SEED_STACK, tokens, d)
+    s = synth.matrix_seed(synth.SEED_STACK + 100, 0, 1)
+    qw, sc = synth.random_packed_bytes(s, d, d), synth.random_scales_f16(s, d, d // 128)
+    x = synth.activations_bf16(synth.SEED_STACK + 100, tokens, d)
     t0 = time.perf_counter()
-    O.stack_layer(h, layer)
-    t = time.perf_counter() - t0
-    pairs_per_s = (tokens / TOKENS_PER_PAIR) / (layers * t)
-    return {"value": round(pairs_per_s, 8), "unit": "pairs/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"one 175B-width block over {tokens} tokens took {t:.1f} s; "
-                      f"pairs/s = ({tokens}/512) / ({layers} x block time)"}
+    O.dequant(qw, sc)
+    t_dq = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.qlinear_ref(x, qw, sc)
+    t_ref = time.perf_counter() - t0
+    if limiter is not None:
+        limiter.restore_original_limits()
+    t_mm = max(t_ref - t_dq, 0.0)
+    block_weights = 3 * d * d + d * d + 2 * d * dff
+    scale = block_weights / (d * d)              # 12 for the 175B shape
+    forward_s = layers * scale * (t_dq + t_mm)
+    pairs = tokens / TOKENS_PER_PAIR
+    return {"value": round(pairs / forward_s, 8), "unit": "pairs/s",
+            "cores": int(blas_threads or affinity), "kind": "oracle",
+            "sample": f"oracle on the out projection (12288 x 12288) over {tokens} tokens: "
+                      f"dequant {t_dq:.2f} s, fp64 product {t_mm:.2f} s; forward = "
+                      f"{layers} blocks x {scale:g} x (dequant + product), extrapolated",
+            "oracle_dequant_s": round(t_dq, 3), "oracle_matmul_s": round(t_mm, 3),
+            "extrapolated_forward_s": round(forward_s, 1),
+            "os_cpu_count": cpu_count, "sched_affinity": affinity,
+            "blas_threads": blas_threads}
 
 
 def main():

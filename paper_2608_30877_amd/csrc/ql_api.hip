@@ -506,17 +506,25 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
   ql_layer dev[2];
   for (int k = 0; k < 2; ++k) dev[k] = slot_layer(static_cast<char*>(slots) + k * S.total, S);
   // copied[k]: slot k holds the layer the next block reads; freed[k]: the
-  // block that last read slot k has finished
-  hipEvent_t copied[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
+  // block that last read slot k has finished; entry: everything enqueued on
+  // `stream` before this call (an earlier call's blocks may still read the
+  // slots, and the residual stream may still be in flight)
+  hipEvent_t copied[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr}, entry = nullptr;
   int out = QL_OK;
   for (int k = 0; k < 2 && out == QL_OK; ++k)
     if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&freed[k], hipEventDisableTiming) != hipSuccess)
       out = QL_ERR_HIP;
+  if (out == QL_OK && hipEventCreateWithFlags(&entry, hipEventDisableTiming) != hipSuccess)
+    out = QL_ERR_HIP;
   auto copy_layer = [&](int l, int k) -> hipError_t {
     hipError_t e = copy_matrices(host_layers[l], dev[k], d, d_ff, cs);
     return e != hipSuccess ? e : hipEventRecord(copied[k], cs);
   };
+  // the first copy into the slots waits for the work already on `stream`
+  if (out == QL_OK && (hipEventRecord(entry, s) != hipSuccess ||
+                       hipStreamWaitEvent(cs, entry, 0) != hipSuccess))
+    out = QL_ERR_HIP;
   if (out == QL_OK && copy_layer(0, 0) != hipSuccess) out = QL_ERR_HIP;
   for (int l = 0; l < n_layers && out == QL_OK; ++l) {
     const int k = l & 1, nk = k ^ 1;
@@ -535,6 +543,7 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
     if (copied[k]) (void)hipEventDestroy(copied[k]);
     if (freed[k]) (void)hipEventDestroy(freed[k]);
   }
+  if (entry) (void)hipEventDestroy(entry);
   return out;
 }
 

@@ -159,3 +159,36 @@ def random_scales_f16(seed: int, N: int, G: int, lo: float = 0.004, hi: float = 
     N(0, 0.02) weights give), for packed weights drawn directly as bytes."""
     v = _rng(seed + 10_000_000).uniform(lo, hi, size=(N, G)).astype(np.float32)
     return v.astype(np.float16).view(np.uint16)
+
+
+def pow2_scales_f16(seed: int, N: int, G: int, e_lo: int = 2, e_hi: int = 6) -> np.ndarray:
+    """[N, G] binary16 bits of 2^-e, e drawn uniformly from e_lo..e_hi for
+    every (column, group) on its own.  With ternary activations and uniform
+    codes every partial sum of the projection stays an exact fp32 value (up
+    to K = 49152 for the default range), so outputs are exact in any
+    summation order while each group still has a scale of its own."""
+    e = _rng(seed + 14_000_000).integers(e_lo, e_hi + 1, size=(N, G))
+    return (0x3C00 - (e << 10)).astype(np.uint16)
+
+
+def pow2_scales_f16_cuda(seed: int, N: int, G: int, e_lo: int = 2, e_hi: int = 6):
+    """pow2_scales_f16's distribution drawn on the current CUDA device with
+    torch's seeded generator: [N, G] int16 bit patterns."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    e = torch.randint(e_lo, e_hi + 1, (N, G), dtype=torch.int32, device="cuda", generator=g)
+    return (0x3C00 - (e << 10)).to(torch.int16)
+
+
+def random_scales_f16_cuda(seed: int, N: int, G: int, lo: float = 0.004, hi: float = 0.016):
+    """random_scales_f16's distribution drawn on the current CUDA device:
+    [N, G] int16 bit patterns of fp16 scales uniform in [lo, hi]."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    t = torch.empty((N, G), dtype=torch.float32, device="cuda")
+    t.uniform_(lo, hi, generator=g)
+    return t.to(torch.float16).view(torch.int16)

@@ -119,11 +119,14 @@ def _forward_np(ql, x, qw, sc):
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
 def test_forward_exact_arithmetic_bit_exact(ql, M, N, K):
-    """x in {-1,0,1}, uniform codes, s = 2^-3: out == bf16(int matmul / 8)."""
+    """x in {-1,0,1}, uniform codes, a power-of-two scale 2^-2 .. 2^-6 of its
+    own for every (column, group): every partial sum is exact, so out must
+    equal the oracle's bf16 result bit for bit, which pins which scale each
+    kernel applies to which column and group, across tile edges and tails."""
     say(f"exact M={M} N={N} K={K}")
     x = synth.ternary_bf16(M * 7 + N, M, K)
     qw = synth.random_packed_bytes(M + N * 3, N, K)
-    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    sc = synth.pow2_scales_f16(M + N * 5, N, K // 128)
     ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
     np.testing.assert_array_equal(_forward_np(ql, x, qw, sc), ref)
 
@@ -144,7 +147,7 @@ def test_small_batch_unaligned_scales(ql):
     say(f"unaligned scales M={M} N={N} K={K}")
     x = synth.ternary_bf16(5, M, K)
     qw = synth.random_packed_bytes(6, N, K)
-    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    sc = synth.pow2_scales_f16(6, N, K // 128)
     ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
     buf = torch.zeros(N * (K // 128) + 8, dtype=torch.int16, device="cuda")
     sc_view = buf[1:1 + N * (K // 128)].view(N, K // 128)
@@ -302,6 +305,35 @@ def test_full_ffn_down(ql):
     assert _full_case(ql, 2048, 12288, 49152, synth.SEED_FFN + 1, False, nsamp=48, x=x) <= TOL
 
 
+def test_full_ffn_pair_down_on_gpu_gelu_output(ql):
+    """The FFN pair as the stack runs it, M = 2048: up-projection with the
+    GELU epilogue on the GPU, then the down-projection (K = 49152, N = 12288)
+    on that bf16 output u.  The oracle takes the same u (copied back) and
+    computes the sampled output columns of the down projection, at 5e-3."""
+    M, d, dff = 2048, 12288, 49152
+    say("full FFN pair: down projection on the GPU's own u")
+    x = dev_u16(synth.activations_bf16(synth.SEED_FFN, M, d))
+    qu = synth.random_packed_bytes_cuda(synth.matrix_seed(synth.SEED_FFN, 1, 2), dff, d)
+    su = synth.random_scales_f16_cuda(synth.matrix_seed(synth.SEED_FFN, 1, 2), dff, d // 128)
+    u = torch.empty((M, dff), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(ql.workspace_bytes(M, d), dtype=torch.uint8, device="cuda")
+    ql.forward_ex(x, qu, su, u, ql.EPI_GELU, ws)
+    del qu, su, ws
+    qd = synth.random_packed_bytes_cuda(synth.matrix_seed(synth.SEED_FFN, 1, 3), d, dff)
+    sd = synth.random_scales_f16_cuda(synth.matrix_seed(synth.SEED_FFN, 1, 3), d, dff // 128)
+    y = ql.forward(u, qd, sd)
+    torch.cuda.synchronize()
+    cols = _sampled(d, 48, 77)
+    ci = torch.from_numpy(cols).cuda()
+    u_h = host_u16(u)
+    ref = O.qlinear_ref(u_h, qd[ci].cpu().numpy(), host_u16(sd[ci]))
+    err = O.rel_fro(bf16_as_f64(host_u16(y[:, ci])), ref)
+    say(f"  down on u: rel err {err:.3e}")
+    assert err <= TOL
+    del x, u, qd, sd, y
+    torch.cuda.empty_cache()
+
+
 def test_full_small_batch(ql):
     """Bandwidth-bound regime: M = 8, K = 12288, N = 49152."""
     assert _full_case(ql, 8, 49152, 12288, synth.SEED_GEMV, False, nsamp=512) <= TOL
@@ -309,12 +341,14 @@ def test_full_small_batch(ql):
 
 @pytest.mark.parametrize("M,N,K", [(2048, 12288, 49152), (8, 49152, 12288)])
 def test_full_exact_arithmetic_bit_exact(ql, M, N, K):
-    """Exact-arithmetic inputs at full size (K = 49152 is the longest
-    reduction: partial sums stay below 2^24 quanta of 2^-3)."""
+    """Exact-arithmetic inputs at full size with per-(column, group) scales
+    2^-2 .. 2^-6.  K = 49152 is the longest reduction: |sum x q| <= 1024 per
+    group, so the output stays below 384 * 1024 * 2^4 = 6.3e6 < 2^24 quanta
+    of 2^-6 and every partial sum is exact."""
     say(f"full exact M={M} N={N} K={K}")
     x = synth.ternary_bf16(9, M, K)
     qw = synth.random_packed_bytes(9, N, K)
-    sc = synth.const_f16_bits(N, K // 128, 0x3000)
+    sc = synth.pow2_scales_f16(9, N, K // 128)
     y = ql.forward(dev_u16(x), dev(qw), dev_u16(sc))
     torch.cuda.synchronize()
     cols = _sampled(N, 64, 9)
@@ -332,7 +366,7 @@ def test_max_size_launch_split_bit_exact(ql, M, N, K):
     say(f"max-size split M={M} N={N} K={K}")
     x = synth.ternary_bf16_cuda(31, M, K)
     qw = synth.random_packed_bytes_cuda(32, N, K)
-    sc = dev_u16(synth.const_f16_bits(N, K // 128, 0x3000))
+    sc = synth.pow2_scales_f16_cuda(33, N, K // 128)
     y = ql.forward(x, qw, sc)
     torch.cuda.synchronize()
     rows_lim = (2 ** 31 // (K * 2)) // 128 * 128      # row chunk of the split
@@ -347,10 +381,9 @@ def test_max_size_launch_split_bit_exact(ql, M, N, K):
     ri = torch.from_numpy(rows).cuda()
     ci = torch.from_numpy(cols).cuda()
     xs = host_u16(x[ri])
-    ref = O.f64_to_bf16_bits(O.qlinear_ref(xs, qw[ci].cpu().numpy(),
-                                           synth.const_f16_bits(len(cols), K // 128, 0x3000)))
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(xs, qw[ci].cpu().numpy(), host_u16(sc[ci])))
     np.testing.assert_array_equal(host_u16(y[ri][:, ci]), ref)
-    del x, qw, y
+    del x, qw, sc, y
     torch.cuda.empty_cache()
 
 

@@ -97,25 +97,31 @@ def test_streamed_larger_blocks_equal_resident(ql):
 
 
 def test_streamed_back_to_back_calls(ql):
-    """Two calls in a row on the same slots with different weights: each
-    equals its resident result."""
-    d, dff, M = 256, 1024, 40
+    """Two calls in a row on the same slots and stream with different
+    weights, enqueued with no synchronisation between them (the second
+    call's first copies must wait for the first call's last blocks): each
+    equals its resident result, computed beforehand."""
+    d, dff, M, L = 256, 1024, 40, 3
     ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
     slots = torch.empty(2 * ql.stack_slot_bytes(d, dff), dtype=torch.uint8, device="cuda")
     cs = torch.cuda.Stream()
-    keep = []
-    outs = []
+    cases = []
     for seed in (63, 64):
-        layers = [_layer_np(seed, l, d, dff) for l in range(3)]
+        layers = [_layer_np(seed, l, d, dff) for l in range(L)]
         h0 = synth.residual_f32(seed, M, d)
         ref = dev(h0)
         ql.stack_forward(ql.make_layers([_on_device(x) for x in layers]), ref, dff, ws)
-        torch.cuda.synchronize()
+        cases.append((layers, h0, ref))
+    torch.cuda.synchronize()
+    keep, outs = [], []
+    for layers, h0, ref in cases:
         host = [_pinned(x) for x in layers]
         keep.append(host)
         b = dev(h0)
-        ql.stack_forward_streamed(ql.make_layers(host), b, dff, ws, slots, cs)
         outs.append((ref, b))
+    torch.cuda.synchronize()   # inputs in place; nothing below synchronises
+    for (layers, h0, ref), host, (_, b) in zip(cases, keep, outs):
+        ql.stack_forward_streamed(ql.make_layers(host), b, dff, ws, slots, cs)
     torch.cuda.synchronize()
     for ref, b in outs:
         assert torch.equal(ref, b)

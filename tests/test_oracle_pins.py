@@ -479,3 +479,27 @@ def test_attention_rows_match_the_full_attention():
         rows = list(range(M))
         got = O.attention_rows_ref(bits, d, heads, L, window, rows)
         np.testing.assert_allclose(got, full, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------------ checker and scale indexing
+
+def test_rel_fro_closed_forms():
+    """The relative Frobenius error that every tolerance test uses."""
+    from tests.oracle_checks import check_rel_fro
+
+    check_rel_fro(O.rel_fro)
+
+
+def test_rmsnorm_eps_and_mean_closed_forms():
+    """RMSNorm's eps inside the square root, the mean over d, unit gain:
+    rows whose bf16 result changes with each of them (exact to 60 digits)."""
+    from tests.oracle_checks import check_rmsnorm
+
+    check_rmsnorm(O.rmsnorm_bf16)
+
+
+def test_per_group_scales_exact():
+    """A scale of its own per (column, group): exact rational sums."""
+    from tests.oracle_checks import check_per_group_scales
+
+    check_per_group_scales(O.qlinear_ref, O.unpack_codes)
