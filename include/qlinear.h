@@ -25,7 +25,12 @@
  *     current device) unless the comment says "host".  The caller owns every
  *     buffer; the library never frees a caller buffer.
  *   - Calls enqueue work on `stream` (NULL = the default stream) and return
- *     without synchronising.  On a non-zero return nothing was enqueued.
+ *     without synchronising.  Arguments are validated before anything is
+ *     enqueued, so QL_ERR_ARG, QL_ERR_UNSUPPORTED, QL_ERR_ALIGN and
+ *     QL_ERR_WORKSPACE mean nothing was enqueued.  QL_ERR_HIP reports a
+ *     failed launch or runtime call; work enqueued before it (earlier
+ *     kernels of the same call) may still run, and the outputs are then
+ *     unspecified.
  *   - Shapes: M, N >= 1; K >= 128 and K % 128 == 0; group must be 128
  *     (other group sizes return QL_ERR_UNSUPPORTED).  Ragged M and N are
  *     handled by masking; no padding is required of the caller.
@@ -94,10 +99,10 @@ int qlinear_dequant(const uint8_t* qweight, const uint16_t* scales, float* w,
  * qlinear_forward -- out[M][N] = bf16(x[M][K] * W_dq^T), the quantized
  * linear projection of Sec. 3.3's "batch molecular encoding" forward pass.
  * M <= 16 runs the bandwidth-bound small-batch kernel, larger M the
- * MFMA tile kernel.  Uses a library-owned device workspace (grown on
- * demand, one per device and stream, kept until qlinear_release); a call
- * that must grow it synchronises `stream` and may allocate.  Callers that
- * cannot allocate use qlinear_forward_ex with their own workspace.
+ * MFMA tile kernel directly on x (each workgroup derives the per-group
+ * activation sums it needs).  Allocates nothing, keeps no state between
+ * calls and does not synchronise, so it may be captured in a HIP graph;
+ * calls on different streams are independent.
  *   x    [M][K] bf16 bits, contiguous.
  *   out  [M][N] bf16 bits, contiguous, written.
  */
@@ -106,19 +111,24 @@ int qlinear_forward(const uint16_t* x, const uint8_t* qweight,
                     int64_t M, int64_t N, int64_t K, int32_t group,
                     ql_stream_t stream);
 
-/* Bytes of workspace qlinear_forward_ex needs for an M x K input. */
+/* Bytes of the optional workspace of qlinear_forward_ex for an M x K input
+ * (0 when the small-batch kernel serves the shape). */
 size_t qlinear_workspace_bytes(int64_t M, int64_t K, int32_t group);
 
 /*
- * qlinear_forward_ex -- qlinear_forward with strides, a fused epilogue and a
- * caller-owned workspace; never allocates.
+ * qlinear_forward_ex -- qlinear_forward with strides, a fused epilogue and
+ * an optional caller-owned workspace; never allocates.
  *   x          bf16 bits, row m at x + m*ldx (ldx >= K elements).
  *   out        QL_EPI_NONE / QL_EPI_GELU: bf16 bits, row m at out + m*ldo
  *              (uint16 elements).  QL_EPI_RESID_F32: fp32, row m at
  *              (float*)out + m*ldo, read and updated in place.
- *   workspace  device buffer of at least qlinear_workspace_bytes(M, K, g)
- *              bytes, 256-byte aligned, used only while the enqueued work
- *              runs; calls that overlap on one workspace race.
+ *   workspace  NULL (ws_bytes ignored): the MFMA kernel reads x as stored,
+ *              as in qlinear_forward.  Otherwise a device buffer of at least
+ *              qlinear_workspace_bytes(M, K, g) bytes, 256-byte aligned
+ *              (QL_ERR_WORKSPACE / QL_ERR_ALIGN): x is first rewritten there
+ *              in the kernel's operand layout with its per-group sums; used
+ *              only while the enqueued work runs; calls that overlap on one
+ *              workspace race.
  */
 int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
                        const uint16_t* scales, void* out, int64_t ldo,
@@ -313,10 +323,6 @@ void qlayer_stack_workspace_offsets(int64_t M, int64_t d, int64_t d_ff,
  */
 int qlinear_rmsnorm(const float* h, uint16_t* a, int64_t M, int64_t d,
                     float eps, ql_stream_t stream);
-
-/* Frees the library-owned workspaces of qlinear_forward (synchronises the
- * device first).  Safe to call at any time; later calls re-create them. */
-void qlinear_release(void);
 
 #ifdef __cplusplus
 }

@@ -19,7 +19,7 @@ __all__ = [
     "LIB_PATH", "QLError", "lib", "GROUP", "EPI_NONE", "EPI_GELU", "EPI_RESID_F32",
     "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
-    "stack_forward_timed", "make_layers", "release", "attention", "attention_varlen",
+    "stack_forward_timed", "make_layers", "attention", "attention_varlen",
     "stack_slot_bytes", "stack_forward_streamed",
 ]
 
@@ -66,7 +66,6 @@ def _load():
                                                     i32, i32, vp]),
         "qlayer_stack_forward_attn": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
                                                      ctypes.c_float, vp, vp, sz, vp, vp]),
-        "qlinear_release": (None, []),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -196,9 +195,10 @@ def workspace_bytes(M: int, K: int, group: int = GROUP) -> int:
 def forward_ex(x, qweight, scales, out, epilogue: int = EPI_NONE, workspace=None,
                M=None, N=None, K=None, ldx=None, ldo=None, group: int = GROUP, stream=None,
                x_ptr=None):
-    """Strided / fused-epilogue forward with a caller workspace (uint8 tensor).
-    x may be a strided 2-D view (row stride ldx); out is bf16 for NONE/GELU
-    and fp32 (updated in place) for RESID_F32."""
+    """Strided / fused-epilogue forward with an optional caller workspace
+    (uint8 tensor; None runs the MFMA kernel on x as stored).  x may be a
+    strided 2-D view (row stride ldx); out is bf16 for NONE/GELU and fp32
+    (updated in place) for RESID_F32."""
     M = x.shape[0] if M is None else M
     K = x.shape[1] if K is None else K
     N = qweight.shape[0] if N is None else N
@@ -366,6 +366,3 @@ def stack_forward_streamed(host_layers_arr, h: torch.Tensor, d_ff: int, workspac
     _check(rc, "qlayer_stack_forward_streamed")
     return h
 
-
-def release():
-    lib.qlinear_release()

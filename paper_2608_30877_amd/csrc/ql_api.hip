@@ -1,10 +1,5 @@
 // C ABI of libqlinear: argument validation, dispatch between the small-batch
-// and MFMA kernels, the library-owned workspaces of qlinear_forward, and the
-// host driver of the 175B-shaped linear stack.
-#include <map>
-#include <mutex>
-#include <utility>
-
+// and MFMA kernels, and the host driver of the 175B-shaped linear stack.
 #include "../../include/qlinear.h"
 #include "ql_internal.h"
 
@@ -31,49 +26,20 @@ size_t forward_ws_bytes(int64_t M, int64_t K) {
   return xp_bytes(M, K) + ns_bytes(M, K);
 }
 
-// dispatch on prepared / raw operands; workspace already validated
+// dispatch: small batches run the small-batch kernel; otherwise the MFMA
+// kernel on the operand prepared in the workspace, or, without one, on the
+// activations as stored.  Workspace already validated.
 int run_linear(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc, void* out,
                int64_t ldo, int64_t M, int64_t N, int64_t K, int epi, void* ws,
                hipStream_t s) {
   if (use_gemv(M, K)) return hip_status(launch_gemv(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
+  if (!ws) return hip_status(launch_gemm_raw(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
   uint16_t* xp = static_cast<uint16_t*>(ws);
   float* ns = reinterpret_cast<float*>(static_cast<char*>(ws) + xp_bytes(M, K));
   const int64_t Mp = padded_rows(M);
   hipError_t e = launch_prep(x, ldx, xp, ns, M, K, Mp, s);
   if (e != hipSuccess) return QL_ERR_HIP;
   return hip_status(launch_gemm(xp, ns, Mp, qw, sc, out, ldo, M, N, K, epi, s));
-}
-
-// ---- library-owned workspaces for qlinear_forward: one per (device, stream)
-struct OwnedWs {
-  void* ptr = nullptr;
-  size_t bytes = 0;
-};
-std::mutex g_ws_mu;
-std::map<std::pair<int, hipStream_t>, OwnedWs> g_ws;
-
-int owned_workspace(hipStream_t s, size_t need, void** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return QL_ERR_HIP;
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  OwnedWs& w = g_ws[{dev, s}];
-  if (w.bytes < need) {
-    if (w.ptr) {
-      // work already queued on this stream may still read the old buffer
-      if (hipStreamSynchronize(s) != hipSuccess) return QL_ERR_HIP;
-      if (hipFree(w.ptr) != hipSuccess) return QL_ERR_HIP;
-      w.ptr = nullptr;
-      w.bytes = 0;
-    }
-    size_t grow = need + need / 4;
-    if (hipMalloc(&w.ptr, grow) != hipSuccess) {
-      w.ptr = nullptr;
-      return QL_ERR_HIP;
-    }
-    w.bytes = grow;
-  }
-  *out = w.ptr;
-  return QL_OK;
 }
 
 // ---- stack workspace layout
@@ -364,8 +330,10 @@ int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
     return QL_ERR_ALIGN;
   if ((ldx * 2) % 16) return QL_ERR_ALIGN;
   const size_t need = forward_ws_bytes(M, K);
-  if (need) {
-    if (!workspace || ws_bytes < need) return QL_ERR_WORKSPACE;
+  if (!need || !workspace) {
+    workspace = nullptr;  // small batch, or the MFMA kernel on x as stored
+  } else {
+    if (ws_bytes < need) return QL_ERR_WORKSPACE;
     if (!aligned256(workspace)) return QL_ERR_ALIGN;
   }
   return run_linear(x, ldx, qweight, scales, out, ldo, M, N, K, epilogue, workspace,
@@ -380,13 +348,7 @@ int qlinear_forward(const uint16_t* x, const uint8_t* qweight, const uint16_t* s
   if (rc) return rc;
   if (!aligned16(x) || !aligned16(qweight) || ((uintptr_t)out & 1u) || ((uintptr_t)scales & 1u))
     return QL_ERR_ALIGN;
-  const size_t need = forward_ws_bytes(M, K);
-  void* ws = nullptr;
-  if (need) {
-    rc = owned_workspace((hipStream_t)stream, need, &ws);
-    if (rc) return rc;
-  }
-  return run_linear(x, K, qweight, scales, out, N, M, N, K, QL_EPI_NONE, ws,
+  return run_linear(x, K, qweight, scales, out, N, M, N, K, QL_EPI_NONE, nullptr,
                     (hipStream_t)stream);
 }
 
@@ -545,21 +507,6 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
   }
   if (entry) (void)hipEventDestroy(entry);
   return out;
-}
-
-void qlinear_release(void) {
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  if (!g_ws.empty()) (void)hipDeviceSynchronize();
-  for (auto& kv : g_ws) {
-    if (kv.second.ptr) {
-      int cur = 0;
-      (void)hipGetDevice(&cur);
-      (void)hipSetDevice(kv.first.first);
-      (void)hipFree(kv.second.ptr);
-      (void)hipSetDevice(cur);
-    }
-  }
-  g_ws.clear();
 }
 
 }  // extern "C"

@@ -57,6 +57,21 @@ __device__ __forceinline__ bf16x8 unpack_offset_codes(uint32_t w) {
   return __builtin_bit_cast(bf16x8, d);
 }
 
+// The same 8 codes in natural k order: dword i holds (136 + q[2i], 136 + q[2i+1]),
+// matching an activation chunk read as stored.  Byte i of w holds q[2i] (low
+// nibble) and q[2i+1] (high nibble); a byte permute places byte i of w in the
+// low half and byte i of w >> 4 in the high half, then the mask / XOR of
+// unpack_offset_codes applies.
+__device__ __forceinline__ bf16x8 unpack_offset_codes_natural(uint32_t w) {
+  const uint32_t w4 = w >> 4;
+  u32x4 d;
+  d.x = (__builtin_amdgcn_perm(w4, w, 0x04040000u) & 0x000f000fu) ^ 0x43084308u;
+  d.y = (__builtin_amdgcn_perm(w4, w, 0x05050101u) & 0x000f000fu) ^ 0x43084308u;
+  d.z = (__builtin_amdgcn_perm(w4, w, 0x06060202u) & 0x000f000fu) ^ 0x43084308u;
+  d.w = (__builtin_amdgcn_perm(w4, w, 0x07070303u) & 0x000f000fu) ^ 0x43084308u;
+  return __builtin_bit_cast(bf16x8, d);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // bf16 -136.0 in both halves of every dword.

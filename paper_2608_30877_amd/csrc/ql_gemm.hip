@@ -19,6 +19,15 @@
 //     FMA applies the group's scale: acc += chain * s[n][g].  That FMA is
 //     issued one fragment later, so it never waits on the chain's last MFMA.
 // Scales therefore stay exact fp32 (no bf16 rounding of q*s).
+//
+// Two operand forms.  Prepared (RAW = false): the activations arrive
+// k-permuted in 8-element chunks with their corrections alongside (written
+// by launch_prep or by the producing kernel's epilogue).  Raw (RAW = true):
+// the activations are read as stored, the codes are unpacked in natural k
+// order, and each wave derives the corrections of the 16 rows it copies
+// itself -- one more 4-MFMA chain per group against a constant -136
+// operand, run on the next group's rows before the step barrier, so the
+// call needs no staging buffer at all.
 #include <algorithm>
 
 #include "ql_device.h"
@@ -57,12 +66,12 @@ struct TileM {
 };
 
 struct GemmParams {
-  const uint16_t* xp;
-  const float* ns;
+  const uint16_t* xp;  // prepared operand (row stride K), or raw x (row stride ldx)
+  const float* ns;     // corrections of the prepared operand (unused when raw)
   const uint8_t* qw;
   const uint16_t* sc;
   void* out;  // may be null when only the prepared copy is wanted
-  int64_t ldo, Mp;
+  int64_t ldo, Mp, ldx;
   int M, N, K, G;
   int tiles_m, tiles_n;
   // prepared copy of output columns >= pcol0 (see GemmPrep)
@@ -187,13 +196,21 @@ struct Offsets {
 // Copies of group g into stage st.  Waves 0-1 copy the BM correction terms
 // (rows past BM repeat the last one), waves 2-5 the 256 scales, each first;
 // then every wave issues kLaterCopies activation / code copies.
-template <int IF>
+// 64-slot block (4 rows of the activation tile) that copy j of a wave fills:
+// interleaved over the waves for the prepared form; for the raw form wave w
+// fills rows 16w .. 16w + 15, the row fragment whose corrections it derives.
+template <int IF, bool RAW>
+__device__ __forceinline__ int a_block(int j, int wave) {
+  return RAW ? wave * TileM<IF>::A_PER_WAVE + j : j * NW + wave;
+}
+
+template <int IF, bool RAW>
 __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
                                             int64_t m0, int g, const Stage& st, int wave, int lane) {
   constexpr int BM = TileM<IF>::BM;
   const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
   const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
-  if (wave * 64 < BM)
+  if (!RAW && wave * 64 < BM)
     copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + min(wave * 64 + lane, BM - 1), st.N + wave * 64);
   else if (wave >= 2 && wave < 6)
     copy_to_lds<2>(p.sc + os + g, st.S + (wave - 2) * 64);
@@ -204,7 +221,7 @@ __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<I
 #pragma unroll
   for (int j = 0; j < NA; ++j) {
     asrc[j] = xa + o.a[j];
-    alds[j] = (uint32_t)reinterpret_cast<uintptr_t>(st.A + (j * NW + wave) * 64);
+    alds[j] = (uint32_t)reinterpret_cast<uintptr_t>(st.A + a_block<IF, RAW>(j, wave) * 64);
   }
   copy16_to_lds<NA>(asrc, alds, qb + o.b[0],
                     (uint32_t)reinterpret_cast<uintptr_t>(st.B + (0 * NW + wave) * 64), qb + o.b[1],
@@ -300,17 +317,44 @@ __device__ __forceinline__ void load_a(const Stage& st, int i, int h, int lr, bf
   n4 = *reinterpret_cast<const f32x4*>(st.N + i * 16 + h * 4);
 }
 
+template <bool RAW>
 __device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
                                        bf16x8 (&bq)[JF][4]) {
 #pragma unroll
   for (int j = 0; j < JF; ++j) {
     const int col = wave * WN + j * 16 + lr;
     const u32x4 raw = st.B[col * 4 + (h ^ b_swz(col))];
-    bq[j][0] = unpack_offset_codes(raw.x);
-    bq[j][1] = unpack_offset_codes(raw.y);
-    bq[j][2] = unpack_offset_codes(raw.z);
-    bq[j][3] = unpack_offset_codes(raw.w);
+    if constexpr (RAW) {
+      bq[j][0] = unpack_offset_codes_natural(raw.x);
+      bq[j][1] = unpack_offset_codes_natural(raw.y);
+      bq[j][2] = unpack_offset_codes_natural(raw.z);
+      bq[j][3] = unpack_offset_codes_natural(raw.w);
+    } else {
+      bq[j][0] = unpack_offset_codes(raw.x);
+      bq[j][1] = unpack_offset_codes(raw.y);
+      bq[j][2] = unpack_offset_codes(raw.z);
+      bq[j][3] = unpack_offset_codes(raw.w);
+    }
   }
+}
+
+// Raw form: corrections -136 * sum_k x[m][k] of the group in stage st for
+// the 16 rows of row fragment `wave` (copied by this wave), as a chain of
+// four MFMAs against a constant -136 operand (every column of the result
+// holds the row's sum).
+__device__ __forceinline__ f32x4 row_corrections(const Stage& st, int wave, int h, int lr) {
+  const int row = wave * 16 + lr;
+  const bf16x8 neg = neg136x8();
+  f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 4; ++s) c = mfma16x16x32(as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]), neg, c);
+  return c;
+}
+
+// lanes of column 0 hold rows 4h .. 4h + 3 of the fragment
+__device__ __forceinline__ void store_corrections(const Stage& st, int wave, int h, int lr,
+                                                  const f32x4& c) {
+  if (lr == 0) *reinterpret_cast<f32x4*>(st.N + wave * 16 + h * 4) = c;
 }
 
 // One group.  On entry bq holds the group's unpacked codes and (a, n4) its
@@ -320,21 +364,29 @@ __device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
 // last fragment every read of `cur` is complete, so the wave waits for its
 // copies of the next group and joins the step barrier; the next group's
 // codes and fragment 0 are then read from `nxt` under fragment 7's MFMAs.
-template <int IF>
+// Raw form: the wave's own copies of the next group land before fragment
+// IF - 2 (the wait moves there), the correction chain of its rows is issued
+// ahead of that fragment's MFMAs and stored after them, before the barrier.
+template <int IF, bool RAW>
 __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt, int wave,
                                               int lane, bf16x8 (&bq)[JF][4], bf16x8 (&a)[4],
                                               f32x4& n4, f32x4 (&cprev)[JF], float (&sprev)[JF],
                                               f32x4 (&acc)[IF][JF]) {
+  static_assert(!RAW || IF >= 2, "raw form needs two fragments per stage");
   const int h = lane >> 4, lr = lane & 15;
   float scf[JF];
 #pragma unroll
   for (int j = 0; j < JF; ++j) scf[j] = f16_to_f32((uint16_t)cur.S[wave * WN + j * 16 + lr]);
   bf16x8 an[4];
-  f32x4 nn;
+  f32x4 nn, corr;
 #pragma unroll
   for (int i = 0; i < IF; ++i) {
     if (i + 1 < IF) {
       load_a(cur, i + 1, h, lr, an, nn);
+      if (RAW && i == IF - 2) {
+        __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
+        corr = row_corrections(nxt, wave, h, lr);
+      }
     } else {
       __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
       wg_barrier();
@@ -350,7 +402,9 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
     }
 #pragma unroll
     for (int j = 0; j < JF; ++j) acc[(i + IF - 1) % IF][j] += cprev[j] * sprev[j];
-    if (i == IF - 1) load_b(nxt, wave, h, lr, bq);
+    if (i == IF - 1) load_b<RAW>(nxt, wave, h, lr, bq);
+    // the correction chain was issued ahead of this fragment's MFMAs
+    if (RAW && i == IF - 2) store_corrections(nxt, wave, h, lr, corr);
 #pragma unroll
     for (int j = 0; j < JF; ++j) {
       cprev[j] = c[j];
@@ -365,8 +419,9 @@ __device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt
   }
 }
 
-template <int EPI, bool PREP, int IF>
+template <int EPI, bool PREP, int IF, bool RAW>
 __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
+  static_assert(!RAW || (IF == 8 && !PREP), "raw form: 128-row tiles, plain epilogues");
   using TM = TileM<IF>;
   constexpr int BM = TM::BM;
   __shared__ u32x4 sA0[TM::A_SLOTS], sA1[TM::A_SLOTS], sA2[TM::A_SLOTS];
@@ -400,11 +455,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   Offsets<IF> o;
 #pragma unroll
   for (int j = 0; j < TM::A_PER_WAVE; ++j) {
-    const int slot = (j * NW + wave) * 64 + lane;
+    const int slot = a_block<IF, RAW>(j, wave) * 64 + lane;
     const int row = slot >> 4;
     const int chunk = (slot & 15) ^ a_msk(row);
     const int64_t r = min<int64_t>(m0 + row, p.M - 1);
-    o.a[j] = (uint32_t)((r * p.K + chunk * 8) * 2);
+    o.a[j] = (uint32_t)((r * (RAW ? p.ldx : (int64_t)p.K) + chunk * 8) * 2);
   }
 #pragma unroll
   for (int j = 0; j < B_PER_WAVE; ++j) {
@@ -428,9 +483,13 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   // last group so that every step issues the same copies (the surplus ones
   // land in a stage that is not read again)
   const int G = p.G, Gl = p.G - 1;
-  issue_stage(p, o, os, m0, 0, S0, wave, lane);
-  issue_stage(p, o, os, m0, min(1, Gl), S1, wave, lane);
+  issue_stage<IF, RAW>(p, o, os, m0, 0, S0, wave, lane);
+  issue_stage<IF, RAW>(p, o, os, m0, min(1, Gl), S1, wave, lane);
   __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
+  if constexpr (RAW) {
+    store_corrections(S0, wave, h, lr, row_corrections(S0, wave, h, lr));
+    __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
+  }
   wg_barrier();
 
   bf16x8 bq[JF][4], a[4];
@@ -442,18 +501,18 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     cprev[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     sprev[j] = 0.f;
   }
-  load_b(S0, wave, h, lr, bq);
+  load_b<RAW>(S0, wave, h, lr, bq);
   load_a(S0, 0, h, lr, a, n4);
   int g = 0;
   for (;;) {
-    issue_stage(p, o, os, m0, min(g + 2, Gl), S2, wave, lane);
-    compute_stage<IF>(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
+    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S2, wave, lane);
+    compute_stage<IF, RAW>(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
-    issue_stage(p, o, os, m0, min(g + 2, Gl), S0, wave, lane);
-    compute_stage<IF>(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
+    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S0, wave, lane);
+    compute_stage<IF, RAW>(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
-    issue_stage(p, o, os, m0, min(g + 2, Gl), S1, wave, lane);
-    compute_stage<IF>(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
+    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S1, wave, lane);
+    compute_stage<IF, RAW>(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
     if (++g >= G) break;
   }
   // no copy may still be writing LDS when the workgroup retires
@@ -469,11 +528,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   }
 }
 
-template <int EPI, bool PREP, int IF>
+template <int EPI, bool PREP, int IF, bool RAW = false>
 hipError_t launch_if(GemmParams p, hipStream_t s) {
   p.tiles_m = (p.M + TileM<IF>::BM - 1) / TileM<IF>::BM;
   const dim3 grid((unsigned)(p.tiles_m * p.tiles_n));
-  hipLaunchKernelGGL((k_gemm<EPI, PREP, IF>), grid, dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((k_gemm<EPI, PREP, IF, RAW>), grid, dim3(NW * 64), 0, s, p);
   return hipGetLastError();
 }
 
@@ -483,6 +542,32 @@ hipError_t launch_one(const GemmParams& p, int64_t M, hipStream_t s) {
   if (M <= 32) return launch_if<EPI, PREP, 2>(p, s);
   if (M <= 64) return launch_if<EPI, PREP, 4>(p, s);
   return launch_if<EPI, PREP, 8>(p, s);
+}
+
+GemmParams chunk_params(const uint16_t* x, int64_t ldx, const float* ns, int64_t Mp,
+                        const uint8_t* qw, const uint16_t* sc, void* out, int64_t ldo,
+                        int64_t m_s, int64_t n_s, int64_t mrows, int64_t ncols, int64_t M,
+                        int64_t N, int64_t K, size_t esize) {
+  GemmParams p;
+  p.xp = x + m_s * ldx;
+  p.ns = ns ? ns + m_s : nullptr;
+  p.qw = qw + n_s * (K / 2);
+  p.sc = sc + n_s * (K / kGroup);
+  p.out = out ? static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize : nullptr;
+  p.ldo = ldo;
+  p.Mp = Mp;
+  p.ldx = ldx;
+  p.M = (int)std::min(mrows, M - m_s);
+  p.N = (int)std::min(ncols, N - n_s);
+  p.K = (int)K;
+  p.G = (int)(K / kGroup);
+  p.tiles_m = 0;  // set per row extent in launch_if
+  p.tiles_n = (p.N + BN - 1) / BN;
+  p.pout = nullptr;
+  p.pns = nullptr;
+  p.pld = 0;
+  p.pcol0 = 0;
+  return p;
 }
 
 }  // namespace
@@ -498,20 +583,8 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
   const size_t esize = epilogue == 2 ? 4 : 2;
   for (int64_t m_s = 0; m_s < M; m_s += mrows) {
     for (int64_t n_s = 0; n_s < N; n_s += ncols) {
-      GemmParams p;
-      p.xp = xp + m_s * K;
-      p.ns = ns + m_s;
-      p.qw = qw + n_s * (K / 2);
-      p.sc = sc + n_s * (K / kGroup);
-      p.out = out ? static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize : nullptr;
-      p.ldo = ldo;
-      p.Mp = Mp;
-      p.M = (int)std::min(mrows, M - m_s);
-      p.N = (int)std::min(ncols, N - n_s);
-      p.K = (int)K;
-      p.G = (int)(K / kGroup);
-      p.tiles_m = 0;  // set per row extent in launch_if
-      p.tiles_n = (p.N + BN - 1) / BN;
+      GemmParams p = chunk_params(xp, K, ns, Mp, qw, sc, out, ldo, m_s, n_s, mrows, ncols, M, N,
+                                  K, esize);
       p.pout = prep ? prep->out + m_s * prep->ld : nullptr;
       p.pns = prep ? prep->ns + m_s : nullptr;
       p.pld = prep ? prep->ld : 0;
@@ -529,6 +602,29 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
           case 2: e = launch_one<2, false>(p, M, s); break;
           default: e = launch_one<0, false>(p, M, s); break;
         }
+      }
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_gemm_raw(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
+                           void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
+                           hipStream_t s) {
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t mrows = std::max<int64_t>(kGemmBM, (lim / (ldx * 2)) / kGemmBM * kGemmBM);
+  const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
+  const size_t esize = epilogue == 2 ? 4 : 2;
+  for (int64_t m_s = 0; m_s < M; m_s += mrows) {
+    for (int64_t n_s = 0; n_s < N; n_s += ncols) {
+      const GemmParams p = chunk_params(x, ldx, nullptr, 0, qw, sc, out, ldo, m_s, n_s, mrows,
+                                        ncols, M, N, K, esize);
+      hipError_t e;
+      switch (epilogue) {
+        case 1: e = launch_if<1, false, 8, true>(p, s); break;
+        case 2: e = launch_if<2, false, 8, true>(p, s); break;
+        default: e = launch_if<0, false, 8, true>(p, s); break;
       }
       if (e != hipSuccess) return e;
     }

@@ -60,6 +60,12 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
                        int64_t K, int epilogue, hipStream_t s,
                        const GemmPrep* prep = nullptr);
 
+// The MFMA kernel on activations as stored (row stride ldx): it derives the
+// corrections itself and needs no staging buffer (128-row tiles).
+hipError_t launch_gemm_raw(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
+                           void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
+                           hipStream_t s);
+
 // Small-M kernel on raw bf16 activations (M <= kSmallM).  It keeps the
 // workgroup's scales in LDS: gemv_lds_bytes(K) must stay within kGemvMaxLds
 // (K <= 49152); use_gemv picks it for the shapes it serves.

@@ -30,7 +30,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for need in ["qlinear_pack", "qlinear_forward", "qlayer_stack_forward", "qlinear_dequant",
                  "qlinear_forward_ex", "qlinear_workspace_bytes", "qlinear_status_string",
-                 "qlayer_stack_workspace_bytes", "qlinear_rmsnorm", "qlinear_release",
+                 "qlayer_stack_workspace_bytes", "qlinear_rmsnorm",
                  "qlayer_stack_workspace_offsets", "qlinear_attention",
                  "qlayer_stack_forward_attn", "qlinear_attention_varlen",
                  "qlayer_stack_forward_streamed", "qlayer_stack_slot_bytes"]:
@@ -40,6 +40,15 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in declared_functions():
         assert hasattr(lib, name), f"libqlinear.so does not export {name}"
+
+
+def test_forward_path_allocates_nothing():
+    """The forward entry points call no allocator, free, or synchronisation
+    and keep no workspace map (source check of the C ABI file)."""
+    src = open(os.path.join(ROOT, "paper_2608_30877_amd", "csrc", "ql_api.hip")).read()
+    for banned in ("hipMalloc", "hipFree", "hipStreamSynchronize", "hipDeviceSynchronize",
+                   "std::map", "std::mutex"):
+        assert banned not in src, banned
 
 
 def test_status_strings(lib):
@@ -81,8 +90,11 @@ def test_forward_ex_errors_without_launch(lib):
     assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 7, p, 1 << 20, None) == 2
     # ldx smaller than K
     assert f(p, 64, p, p, p, 64, 64, 64, 128, 128, 0, p, 1 << 20, None) == 1
-    # M > 16 needs a workspace
-    assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 0, None, 0, None) == 6
+    # a workspace that is given must be large enough and 256-byte aligned
+    # (without one the MFMA kernel reads x as stored)
+    assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 0, p, 16, None) == 6
+    assert f(p, 128, p, p, p, 64, 64, 64, 128, 128, 0, ctypes.c_void_p(4096 + 16),
+             1 << 20, None) == 3
     ws = lib.qlinear_workspace_bytes
     ws.argtypes = [i64, i64, i32]
     ws.restype = sz

@@ -75,3 +75,35 @@ def test_stack_graph_replay_matches_eager(ql, M, attn):
     torch.cuda.synchronize()
     assert torch.equal(h2, ref)
     del g
+
+
+@pytest.mark.parametrize("M", [2048, 8])
+def test_qlinear_forward_graph_replay_matches_eager(ql, M):
+    """qlinear_forward allocates nothing and never synchronises, so it can be
+    captured: M = 2048 (the MFMA kernel on x as stored) and M = 8 (the
+    small-batch kernel), K = 12288, N = 36864, each replay bit-equal to the
+    eager call."""
+    K, N = 12288, 36864
+    say(f"graph replay of qlinear_forward M={M}")
+    x = dev_u16(synth.activations_bf16(synth.SEED_QKV, M, K, outlier_frac=0.01))
+    qw = synth.random_packed_bytes_cuda(71, N, K)
+    sc = synth.random_scales_f16_cuda(71, N, K // 128)
+    ref = ql.forward(x, qw, sc)
+    torch.cuda.synchronize()
+    y = torch.empty_like(ref)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ql.forward(x, qw, sc, out=y)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        ql.forward(x, qw, sc, out=y)
+    for rep in range(3):
+        y.zero_()                          # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), f"replay {rep} differs from the eager call"
+    del g

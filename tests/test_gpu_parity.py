@@ -117,6 +117,45 @@ def _forward_np(ql, x, qw, sc):
     return host_u16(y)
 
 
+def _forward_ws_np(ql, x, qw, sc):
+    """qlinear_forward_ex with a workspace: the MFMA kernel on the operand
+    prepared in that workspace (the form the stack uses)."""
+    M, K = x.shape
+    xd = dev_u16(x)
+    out = torch.empty((M, qw.shape[0]), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(ql.workspace_bytes(M, K), 256), dtype=torch.uint8, device="cuda")
+    ql.forward_ex(xd, dev(qw), dev_u16(sc), out, ql.EPI_NONE, ws)
+    torch.cuda.synchronize()
+    return host_u16(out)
+
+
+@pytest.mark.parametrize("M,N,K", [s for s in SHAPES if s[0] > 16])
+def test_forward_prepared_operand_exact_bit_exact(ql, M, N, K):
+    """As test_forward_exact_arithmetic_bit_exact, through the prepared
+    operand (permuted copy and correction terms in a workspace) instead of x
+    as stored."""
+    say(f"exact prepared M={M} N={N} K={K}")
+    x = synth.ternary_bf16(M * 7 + N + 1, M, K)
+    qw = synth.random_packed_bytes(M + N * 3 + 1, N, K)
+    sc = synth.pow2_scales_f16(M + N * 5 + 1, N, K // 128)
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
+    np.testing.assert_array_equal(_forward_ws_np(ql, x, qw, sc), ref)
+
+
+@pytest.mark.parametrize("M,N,K", [s for s in SHAPES if s[0] > 16])
+def test_forward_prepared_operand_workload(ql, M, N, K):
+    x = synth.activations_bf16(M + 11 * N + 1, M, K, outlier_frac=0.01)
+    qw, sc = O.quantize_pack(synth.weights_f32(N + 13 * M + 1, N, K))
+    ref = O.qlinear_ref(x, qw, sc)
+    y = bf16_as_f64(_forward_ws_np(ql, x, qw, sc))
+    assert O.rel_fro(y, ref) <= TOL
+    # the raw and prepared forms differ only in how the per-group sums are
+    # formed: both stay within the offset-trick bound of the exact result
+    assert O.rel_fro(y, bf16_as_f64(O.f64_to_bf16_bits(ref))) <= OFFSET_TOL
+    yr = bf16_as_f64(_forward_np(ql, x, qw, sc))
+    assert O.rel_fro(yr, bf16_as_f64(O.f64_to_bf16_bits(ref))) <= OFFSET_TOL
+
+
 @pytest.mark.parametrize("M,N,K", SHAPES)
 def test_forward_exact_arithmetic_bit_exact(ql, M, N, K):
     """x in {-1,0,1}, uniform codes, a power-of-two scale 2^-2 .. 2^-6 of its
@@ -223,10 +262,12 @@ def test_sign_symmetry(ql, M):
     assert O.rel_fro(-b, a) <= OFFSET_TOL
 
 
+@pytest.mark.parametrize("with_ws", [True, False])
 @pytest.mark.parametrize("epi", [1, 2])
 @pytest.mark.parametrize("M", [12, 160])
-def test_forward_ex_epilogues_and_strides(ql, epi, M):
-    """GELU (bf16 out) and fp32 residual-add epilogues, strided x and out."""
+def test_forward_ex_epilogues_and_strides(ql, epi, M, with_ws):
+    """GELU (bf16 out) and fp32 residual-add epilogues, strided x and out,
+    with a workspace (prepared operand) and without (x read as stored)."""
     K, N = 512, 384
     xfull = synth.activations_bf16(M + epi, M, K + 256)
     x = xfull[:, 64:64 + K]
@@ -234,7 +275,8 @@ def test_forward_ex_epilogues_and_strides(ql, epi, M):
     ref = O.qlinear_ref(np.ascontiguousarray(x), qw, sc)
     xd = dev_u16(xfull)
     xv = xd[:, 64:64 + K]
-    ws = torch.empty(max(ql.workspace_bytes(M, K), 1), dtype=torch.uint8, device="cuda")
+    ws = (torch.empty(max(ql.workspace_bytes(M, K), 1), dtype=torch.uint8, device="cuda")
+          if with_ws else None)
     if epi == 1:
         out = torch.zeros((M, N + 64), dtype=torch.bfloat16, device="cuda")
         ql.forward_ex(xv, dev(qw), dev_u16(sc), out[:, :N], ql.EPI_GELU, ws, ldo=N + 64)
