@@ -59,7 +59,8 @@ enum ql_status {
     QL_ERR_ALIGN = 3,        /* a pointer or row stride breaks 16 B alignment  */
     QL_ERR_HIP = 4,          /* a HIP runtime call or a launch failed          */
     QL_ERR_RANGE = 5,        /* pack: non-finite weight or fp16 scale overflow */
-    QL_ERR_WORKSPACE = 6     /* workspace pointer null or smaller than needed  */
+    QL_ERR_WORKSPACE = 6,    /* workspace pointer null or smaller than needed  */
+    QL_ERR_SCRATCH = 7       /* problem larger than the library's fixed scratch */
 };
 
 enum ql_epilogue {
@@ -310,6 +311,29 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
                                   const ql_attention_cfg* attn, void* workspace,
                                   size_t ws_bytes, void* slots, size_t slot_bytes,
                                   ql_stream_t stream, ql_stream_t copy_stream);
+
+/*
+ * qlayer_stack_forward_noalloc -- qlayer_stack_forward for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same kernels and
+ * results, with the workspace in a fixed device array of the library
+ * (qlayer_stack_scratch_capacity() bytes, 128 MiB, one per GPU, held until
+ * the process ends) instead of a caller buffer.  The call allocates and
+ * frees nothing and does not synchronise.
+ *   Limit: qlayer_stack_workspace_bytes(M, d, d_ff, 128) must not exceed the
+ *   capacity, else QL_ERR_SCRATCH and nothing is enqueued (at d = 12288,
+ *   d_ff = 49152 that admits M <= 597 tokens).
+ *   Every call on one GPU shares that GPU's array: calls that overlap on one
+ *   GPU (other streams, other host threads) race and must be serialised by
+ *   the caller.  h, layers and the other arguments as for
+ *   qlayer_stack_forward.
+ */
+int qlayer_stack_forward_noalloc(const ql_layer* layers, int32_t n_layers, float* h,
+                                 int64_t M, int64_t d, int64_t d_ff, int32_t group,
+                                 float eps, ql_stream_t stream);
+
+/* Bytes of the fixed device array behind qlayer_stack_forward_noalloc. */
+size_t qlayer_stack_scratch_capacity(void);
 
 /* Host: byte offsets of the qkv and u buffers inside the stack workspace. */
 void qlayer_stack_workspace_offsets(int64_t M, int64_t d, int64_t d_ff,

@@ -20,7 +20,8 @@ __all__ = [
     "pack", "dequant", "forward", "forward_ex", "workspace_bytes", "rmsnorm",
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
     "stack_forward_timed", "make_layers", "attention", "attention_varlen",
-    "stack_slot_bytes", "stack_forward_streamed",
+    "stack_slot_bytes", "stack_forward_streamed", "stack_forward_noalloc",
+    "stack_scratch_capacity",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
@@ -61,6 +62,9 @@ def _load():
         "qlayer_stack_forward_streamed": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
                                                          ctypes.c_float, vp, vp, sz, vp, sz, vp,
                                                          vp]),
+        "qlayer_stack_forward_noalloc": (ctypes.c_int, [vp, i32, vp, i64, i64, i64, i32,
+                                                        ctypes.c_float, vp]),
+        "qlayer_stack_scratch_capacity": (sz, []),
         "qlinear_attention": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, i32, i32, vp]),
         "qlinear_attention_varlen": (ctypes.c_int, [vp, i64, vp, i64, i64, i64, i32, vp, i32,
                                                     i32, i32, vp]),
@@ -340,6 +344,23 @@ def stack_forward_timed(layers_arr, h: torch.Tensor, d_ff: int, workspace: torch
                                            ctypes.cast(ev_arr, ctypes.c_void_p), _stream(st))
         _check(rc, "qlayer_stack_forward_attn")
     return h
+
+
+def stack_forward_noalloc(layers_arr, h: torch.Tensor, d_ff: int, n_layers: int | None = None,
+                          eps: float = 1e-5, group: int = GROUP, stream=None):
+    """stack_forward with the workspace in the library's fixed device scratch
+    (no caller buffer, no allocation; calls overlapping on one GPU race)."""
+    _need(h, "h", (torch.float32,), 2)
+    M, d = h.shape
+    n = len(layers_arr) if n_layers is None else n_layers
+    rc = lib.qlayer_stack_forward_noalloc(ctypes.cast(layers_arr, ctypes.c_void_p), n, _ptr(h),
+                                          M, d, d_ff, group, eps, _stream(stream))
+    _check(rc, "qlayer_stack_forward_noalloc")
+    return h
+
+
+def stack_scratch_capacity() -> int:
+    return int(lib.qlayer_stack_scratch_capacity())
 
 
 def stack_slot_bytes(d: int, d_ff: int, group: int = GROUP) -> int:

@@ -288,6 +288,8 @@ const char* qlinear_status_string(int status) {
     case QL_ERR_HIP: return "HIP runtime error or launch failure";
     case QL_ERR_RANGE: return "non-finite weight or fp16 scale overflow";
     case QL_ERR_WORKSPACE: return "workspace missing or too small";
+    case QL_ERR_SCRATCH:
+      return "problem needs more than the library's fixed scratch (qlayer_stack_scratch_capacity)";
     default: return "unknown status";
   }
 }

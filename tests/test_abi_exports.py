@@ -56,7 +56,7 @@ def test_status_strings(lib):
     f.restype = ctypes.c_char_p
     f.argtypes = [ctypes.c_int]
     assert f(0) == b"ok"
-    for code in range(1, 7):
+    for code in range(1, 8):
         assert f(code) and f(code) != b"unknown status"
     assert f(99) == b"unknown status"
 
