@@ -30,10 +30,10 @@ TOKENS_PER_PAIR = 512
 
 PROJ = ("qkv", "out", "up", "down")
 # projection -> kernel symbol it launches (epilogue template argument)
-KERNEL_OF = {"qkv": "k_gemm<0, true, 8> (bf16 store + V operand)",
-             "out": "k_gemm<2, false, 8> (fp32 residual add)",
-             "up": "k_gemm<1, true, 8> (GELU + down operand)",
-             "down": "k_gemm<2, false, 8> (fp32 residual add)"}
+KERNEL_OF = {"qkv": "k_gemm<0, true, 8, false> (bf16 store + V operand)",
+             "out": "k_gemm<2, false, 8, false> (fp32 residual add)",
+             "up": "k_gemm<1, true, 8, false> (GELU + down operand)",
+             "down": "k_gemm<2, false, 8, false> (fp32 residual add)"}
 SYMBOL = {v: v.split(" (")[0] for v in KERNEL_OF.values()}
 
 

@@ -2,22 +2,22 @@
 //
 // out[m][n] = sum_g s[n][g] * sum_{k in g} x[m][k] * q[n][k]
 //
-// Each workgroup (8 waves, two per SIMD) owns a 128 x 256 output tile; wave
-// w owns the 128 x 32 column slice [32w, 32w+32).  The K loop walks one
-// 128-wide scale group per step:
-//   * the activation tile (128 rows x 128 k, pre-permuted bf16), the packed
-//     weight tile (256 columns x 64 bytes), the group's 256 scales and 128
-//     correction terms are copied global -> LDS with direct-to-LDS loads into
-//     a three-stage ring: while group g is computed, the copies of groups
-//     g+1 and g+2 are in flight, so each copy has about two steps to land;
-//   * each wave unpacks its 32 x 128 int4 codes once into bf16 values
-//     136 + q (exact; see unpack_offset_codes) and reuses them for all 8
-//     row fragments;
-//   * per 16 x 16 output fragment, a chain of four 16x16x32 MFMAs covers the
-//     group.  The chain starts from the correction -136 * sum_k x[m][k], so
-//     its result is the integer-code dot product sum x*q (fp32), and one fp32
-//     FMA applies the group's scale: acc += chain * s[n][g].  That FMA is
-//     issued one fragment later, so it never waits on the chain's last MFMA.
+// Each workgroup (8 waves, two per SIMD) owns a 128 x 256 output tile; the
+// waves form a 2 x 4 grid, so each owns a 64 x 64 slice.  The K loop walks
+// one 128-wide scale group per step:
+//   * the activation tile (128 rows x 128 k, bf16), the packed weight tile
+//     (256 columns x 64 bytes), the group's 256 scales and 128 correction
+//     terms are copied global -> LDS with direct-to-LDS loads into a
+//     three-stage ring: while group g is computed, the copies of groups g+1
+//     and g+2 are in flight, so each copy has about two steps to land;
+//   * a step runs four 32-k phases; in each, a wave reads its activation
+//     fragments from LDS, unpacks one 32-bit word of codes per column
+//     fragment into bf16 values 136 + q (exact; see unpack_offset_codes) and
+//     issues one 16x16x32 MFMA for each of its 4 x 4 output fragments;
+//   * each fragment's chain of four MFMAs starts from the correction
+//     -136 * sum_k x[m][k], so its result is the integer-code dot product
+//     sum x*q (fp32), and one fp32 FMA applies the group's scale:
+//     acc += chain * s[n][g].
 // Scales therefore stay exact fp32 (no bf16 rounding of q*s).
 //
 // Two operand forms.  Prepared (RAW = false): the activations arrive
@@ -38,9 +38,7 @@ namespace ql {
 namespace {
 
 constexpr int NW = 8;                  // waves per workgroup
-constexpr int WN = 32;                 // columns per wave
-constexpr int JF = WN / 16;            // 16-column fragments per wave
-constexpr int BN = NW * WN;            // 256
+constexpr int BN = 256;                // columns per workgroup tile
 constexpr int B_SLOTS = BN * 4;        // 16-byte slots of codes per stage (16 KB)
 constexpr int B_PER_WAVE = B_SLOTS / 64 / NW;   // 2 direct-to-LDS loads per wave
 static_assert(BN == kGemmBN, "tile width");
@@ -114,63 +112,84 @@ __device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2))
 // the LDS base (one wait state must separate its write from the load that
 // reads it); M0 is a register the compiler reserves, so each sequence saves
 // and restores it instead of clobbering it.
-#define QL_LDS_COPY(OP, A, L) "s_mov_b32 m0, %[" L "]\n\ts_nop 0\n\t" OP " %[" A "], off\n\t"
+// Addresses are a uniform 64-bit base in scalar registers plus a per-lane
+// 32-bit byte offset, so advancing to the next group touches scalar
+// registers only.
+#define QL_LDS_COPY(OP, V, B, L) \
+  "s_mov_b32 m0, %[" L "]\n\ts_nop 0\n\t" OP " %[" V "], %[" B "]\n\t"
 
 // one 2- or 4-byte copy (correction terms, scales)
 template <int BYTES>
-__device__ __forceinline__ void copy_to_lds(const void* src, const void* lds) {
+__device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, const void* lds) {
   const uint32_t l = (uint32_t)reinterpret_cast<uintptr_t>(lds);
   uint32_t saved;
   if constexpr (BYTES == 4) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dword", "a", "l")
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dword", "o", "b", "l")
                  "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved) : [a] "v"(src), [l] "s"(l) : "memory");
+                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
   } else {
     static_assert(BYTES == 2, "copy width");
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_ushort", "a", "l")
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_ushort", "o", "b", "l")
                  "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved) : [a] "v"(src), [l] "s"(l) : "memory");
+                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
   }
 }
 
-// NA 16-byte activation copies then two 16-byte code copies, in one sequence
+// NA 16-byte activation copies (base xa) then two 16-byte code copies (base
+// qb), in one sequence
 template <int NA>
-__device__ __forceinline__ void copy16_to_lds(const void* const (&a)[NA], const uint32_t (&la)[NA],
-                                              const void* b0, uint32_t lb0, const void* b1,
+__device__ __forceinline__ void copy16_to_lds(const void* xa, const uint32_t (&oa)[NA],
+                                              const uint32_t (&la)[NA], const void* qb,
+                                              uint32_t ob0, uint32_t lb0, uint32_t ob1,
                                               uint32_t lb1) {
   uint32_t saved;
 #define QL_X16 "global_load_lds_dwordx4"
   if constexpr (NA == 1) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
-                 QL_LDS_COPY(QL_X16, "b0", "m0v") QL_LDS_COPY(QL_X16, "b1", "m1v")
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
+                 QL_LDS_COPY(QL_X16, "b0", "qb", "m0v") QL_LDS_COPY(QL_X16, "b1", "qb", "m1v")
                  "s_mov_b32 m0, %[sv]"
                  : [sv] "=&s"(saved)
-                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1),
-                   [m1v] "s"(lb1)
+                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [b0] "v"(ob0),
+                   [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
                  : "memory");
   } else if constexpr (NA == 2) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
-                 QL_LDS_COPY(QL_X16, "a1", "l1") QL_LDS_COPY(QL_X16, "b0", "m0v")
-                 QL_LDS_COPY(QL_X16, "b1", "m1v") "s_mov_b32 m0, %[sv]"
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
+                 QL_LDS_COPY(QL_X16, "a1", "xa", "l1") QL_LDS_COPY(QL_X16, "b0", "qb", "m0v")
+                 QL_LDS_COPY(QL_X16, "b1", "qb", "m1v") "s_mov_b32 m0, %[sv]"
                  : [sv] "=&s"(saved)
-                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [a1] "v"(a[1]), [l1] "s"(la[1]),
-                   [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1), [m1v] "s"(lb1)
+                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [a1] "v"(oa[1]),
+                   [l1] "s"(la[1]), [b0] "v"(ob0), [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
                  : "memory");
   } else {
     static_assert(NA == 4, "activation copies per wave");
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "l0")
-                 QL_LDS_COPY(QL_X16, "a1", "l1") QL_LDS_COPY(QL_X16, "a2", "l2")
-                 QL_LDS_COPY(QL_X16, "a3", "l3") QL_LDS_COPY(QL_X16, "b0", "m0v")
-                 QL_LDS_COPY(QL_X16, "b1", "m1v") "s_mov_b32 m0, %[sv]"
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
+                 QL_LDS_COPY(QL_X16, "a1", "xa", "l1") QL_LDS_COPY(QL_X16, "a2", "xa", "l2")
+                 QL_LDS_COPY(QL_X16, "a3", "xa", "l3") QL_LDS_COPY(QL_X16, "b0", "qb", "m0v")
+                 QL_LDS_COPY(QL_X16, "b1", "qb", "m1v") "s_mov_b32 m0, %[sv]"
                  : [sv] "=&s"(saved)
-                 : [a0] "v"(a[0]), [l0] "s"(la[0]), [a1] "v"(a[1]), [l1] "s"(la[1]),
-                   [a2] "v"(a[2]), [l2] "s"(la[2]), [a3] "v"(a[3]), [l3] "s"(la[3]),
-                   [b0] "v"(b0), [m0v] "s"(lb0), [b1] "v"(b1), [m1v] "s"(lb1)
+                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [a1] "v"(oa[1]),
+                   [l1] "s"(la[1]), [a2] "v"(oa[2]), [l2] "s"(la[2]), [a3] "v"(oa[3]),
+                   [l3] "s"(la[3]), [b0] "v"(ob0), [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
                  : "memory");
   }
 #undef QL_X16
 }
 #undef QL_LDS_COPY
+
+// Anchors the computation of v at this point of the program: an empty
+// volatile statement that reads v.  The compiler otherwise moves pure
+// arithmetic (the scale FMAs, the code unpacking) across the scheduling
+// barriers towards its first use, which bunches it up between steps.
+template <class T>
+__device__ __forceinline__ void pin(const T& v) {
+  static_assert(sizeof(T) == 16 || sizeof(T) == 4, "pinned value size");
+  if constexpr (sizeof(T) == 16) {
+    const u32x4 u = __builtin_bit_cast(u32x4, v);
+    asm volatile("" ::"v"(u));
+  } else {
+    asm volatile("" ::"v"(__builtin_bit_cast(uint32_t, v)));
+  }
+}
 
 // Workgroup barrier without the memory fence of __syncthreads (which would
 // also wait for every copy in flight).
@@ -193,9 +212,6 @@ struct Offsets {
   uint32_t b[B_PER_WAVE];             // byte offsets into qw of this lane's B slots (group 0)
 };
 
-// Copies of group g into stage st.  Waves 0-1 copy the BM correction terms
-// (rows past BM repeat the last one), waves 2-5 the 256 scales, each first;
-// then every wave issues kLaterCopies activation / code copies.
 // 64-slot block (4 rows of the activation tile) that copy j of a wave fills:
 // interleaved over the waves for the prepared form; for the raw form wave w
 // fills rows 16w .. 16w + 15, the row fragment whose corrections it derives.
@@ -204,6 +220,9 @@ __device__ __forceinline__ int a_block(int j, int wave) {
   return RAW ? wave * TileM<IF>::A_PER_WAVE + j : j * NW + wave;
 }
 
+// Copies of group g into stage st.  Prepared form: waves 0-1 copy the BM
+// correction terms (rows past BM repeat the last one); both forms: waves 2-5
+// copy the 256 scales; then every wave issues its activation and code copies.
 template <int IF, bool RAW>
 __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
                                             int64_t m0, int g, const Stage& st, int wave, int lane) {
@@ -211,32 +230,42 @@ __device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<I
   const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
   const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
   if (!RAW && wave * 64 < BM)
-    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0 + min(wave * 64 + lane, BM - 1), st.N + wave * 64);
+    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0, (uint32_t)min(wave * 64 + lane, BM - 1) * 4,
+                   st.N + wave * 64);
   else if (wave >= 2 && wave < 6)
-    copy_to_lds<2>(p.sc + os + g, st.S + (wave - 2) * 64);
+    copy_to_lds<2>(p.sc + g, os * 2, st.S + (wave - 2) * 64);
   constexpr int NA = TileM<IF>::A_PER_WAVE;
   static_assert(B_PER_WAVE == 2, "two code copies per wave");
-  const void* asrc[NA];
   uint32_t alds[NA];
 #pragma unroll
-  for (int j = 0; j < NA; ++j) {
-    asrc[j] = xa + o.a[j];
+  for (int j = 0; j < NA; ++j)
     alds[j] = (uint32_t)reinterpret_cast<uintptr_t>(st.A + a_block<IF, RAW>(j, wave) * 64);
-  }
-  copy16_to_lds<NA>(asrc, alds, qb + o.b[0],
-                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (0 * NW + wave) * 64), qb + o.b[1],
+  copy16_to_lds<NA>(xa, o.a, alds, qb, o.b[0],
+                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (0 * NW + wave) * 64), o.b[1],
                     (uint32_t)reinterpret_cast<uintptr_t>(st.B + (1 * NW + wave) * 64));
 }
+
+// Wave layout: the 8 waves form a 2 x 4 grid over the 128 x 256 tile; wave
+// (wr, wc) owns rows wr * BM / 2 .. + BM / 2 (RF = IF / 2 row fragments of 16)
+// and columns 64 wc .. 64 wc + 63 (CF = 4 column fragments of 16).  Compared
+// with waves of 128 x 32, each MFMA needs 41 % fewer LDS bytes (the
+// activation tile is read by 4 waves instead of 8), which is what bounds the
+// loop: every group step reads the stage from LDS at 128 bytes per clock.
+constexpr int WC = 4;            // wave columns
+constexpr int CF = 4;            // 16-column fragments per wave
+static_assert(WC * CF * 16 == BN && NW % WC == 0, "wave grid");
 
 // Epilogue.  EPI 0: bf16 store, 1: GELU then bf16, 2: fp32 residual add.
 // With PREP (EPI 0 or 1) the bf16 values of columns >= pcol0 are also written
 // as the next projection's operand: k-permuted in 8-element chunks, plus the
 // correction ns[g][m] = -136 * (sum of the group's 128 bf16 values of row m),
-// whose per-wave row sums meet in LDS (part) and are added in a fixed order.
+// whose per-wave row sums meet in LDS (part, [WC][BM]) and are added in a
+// fixed order.
 template <int EPI, bool PREP, int IF>
 __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, const f32x4 (&acc)[IF][JF], float* part) {
-  constexpr int BM = TileM<IF>::BM;
+                                           int lane, const f32x4 (&acc)[IF / 2][CF],
+                                           float* part) {
+  constexpr int BM = TileM<IF>::BM, RF = IF / 2;
   if constexpr (PREP) {
     // a tile left of the prepared columns (the Q and K thirds of a QKV
     // projection) is stored plainly, without the row sums and their exchange
@@ -245,20 +274,20 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
       return;
     }
   }
-  const int h = lane >> 4, lr = lane & 15;
-  float rs[IF][4];
+  const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
+  float rs[RF][4];
 #pragma unroll
-  for (int i = 0; i < IF; ++i)
+  for (int i = 0; i < RF; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) rs[i][r] = 0.f;
 #pragma unroll
-  for (int i = 0; i < IF; ++i) {
+  for (int i = 0; i < RF; ++i) {
 #pragma unroll
-    for (int j = 0; j < JF; ++j) {
-      const int64_t col = n0 + wave * WN + j * 16 + lr;
+    for (int j = 0; j < CF; ++j) {
+      const int64_t col = n0 + wc * (CF * 16) + j * 16 + lr;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t row = m0 + i * 16 + h * 4 + r;
+        const int64_t row = m0 + wr * (BM / 2) + i * 16 + h * 4 + r;
         const bool in = col < p.N && row < p.M;
         const float v = acc[i][j][r];
         if constexpr (EPI == 2) {
@@ -280,9 +309,9 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
   }
   if constexpr (PREP) {
     static_assert(EPI != 2, "prepared copy of a residual update");
-    // this wave's 32 columns lie in one 128-column group of the tile
+    // this wave's 64 columns lie in 128-column group wc / 2 of the tile
 #pragma unroll
-    for (int i = 0; i < IF; ++i)
+    for (int i = 0; i < RF; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         // sum over the 16 lanes of a DPP row: quad swaps, then rotations by 4
@@ -292,50 +321,72 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
         t += dpp_f32<0x4E>(t);    // quad_perm [2,3,0,1]
         t += dpp_f32<0x124>(t);   // row_ror:4
         t += dpp_f32<0x128>(t);   // row_ror:8
-        if (lr == 0) part[wave * BM + i * 16 + h * 4 + r] = t;
+        if (lr == 0) part[wc * BM + wr * (BM / 2) + i * 16 + h * 4 + r] = t;
       }
     __syncthreads();
-    // thread t: group t / 128 of the tile, row t % 128
+    // thread t: group t / BM of the tile, row t % BM
     const int t = threadIdx.x;
     if (t < 2 * BM) {
-      const int gg = t / BM, m = t % BM, w0 = gg * (NW / 2);
+      const int gg = t / BM, m = t % BM;
       const int64_t c = n0 + gg * kGroup - p.pcol0;
       if (c >= 0 && n0 + gg * kGroup < p.N) {
-        const float sum = (part[(w0 + 0) * BM + m] + part[(w0 + 1) * BM + m]) +
-                          (part[(w0 + 2) * BM + m] + part[(w0 + 3) * BM + m]);
+        const float sum = part[(2 * gg) * BM + m] + part[(2 * gg + 1) * BM + m];
         p.pns[(c / kGroup) * p.Mp + m0 + m] = -136.0f * sum;
       }
     }
   }
 }
 
-__device__ __forceinline__ void load_a(const Stage& st, int i, int h, int lr, bf16x8 (&a)[4],
-                                       f32x4& n4) {
-  const int row = i * 16 + lr;
+// activations of phase s for the wave's row fragments
+template <int IF>
+__device__ __forceinline__ void read_a(const Stage& st, int wr, int s, int h, int lr,
+                                       bf16x8 (&a)[IF / 2]) {
+  constexpr int BM = TileM<IF>::BM;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) a[s] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
-  n4 = *reinterpret_cast<const f32x4*>(st.N + i * 16 + h * 4);
+  for (int i = 0; i < IF / 2; ++i) {
+    const int row = wr * (BM / 2) + i * 16 + lr;
+    a[i] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
+  }
+}
+
+// the group's codes for the wave's column fragments (16 bytes = 32 codes of
+// column lr per fragment: word s of it feeds phase s)
+__device__ __forceinline__ void read_codes(const Stage& st, int wc, int h, int lr,
+                                           u32x4 (&raw)[CF]) {
+#pragma unroll
+  for (int j = 0; j < CF; ++j) {
+    const int col = wc * (CF * 16) + j * 16 + lr;
+    raw[j] = st.B[col * 4 + (h ^ b_swz(col))];
+  }
 }
 
 template <bool RAW>
-__device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
-                                       bf16x8 (&bq)[JF][4]) {
+__device__ __forceinline__ bf16x8 unpack_word(uint32_t w) {
+  if constexpr (RAW)
+    return unpack_offset_codes_natural(w);
+  else
+    return unpack_offset_codes(w);
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t word(const u32x4& v) {
+  if constexpr (S == 0) return v.x;
+  else if constexpr (S == 1) return v.y;
+  else if constexpr (S == 2) return v.z;
+  else return v.w;
+}
+
+// corrections (chain starts) and scales of a group for the wave's fragments
+template <int IF>
+__device__ __forceinline__ void read_group_terms(const Stage& st, int wr, int wc, int h, int lr,
+                                                 f32x4 (&n4)[IF / 2], f32x4& sc) {
+  static_assert(CF == 4, "one scale per vector element");
+  constexpr int BM = TileM<IF>::BM;
 #pragma unroll
-  for (int j = 0; j < JF; ++j) {
-    const int col = wave * WN + j * 16 + lr;
-    const u32x4 raw = st.B[col * 4 + (h ^ b_swz(col))];
-    if constexpr (RAW) {
-      bq[j][0] = unpack_offset_codes_natural(raw.x);
-      bq[j][1] = unpack_offset_codes_natural(raw.y);
-      bq[j][2] = unpack_offset_codes_natural(raw.z);
-      bq[j][3] = unpack_offset_codes_natural(raw.w);
-    } else {
-      bq[j][0] = unpack_offset_codes(raw.x);
-      bq[j][1] = unpack_offset_codes(raw.y);
-      bq[j][2] = unpack_offset_codes(raw.z);
-      bq[j][3] = unpack_offset_codes(raw.w);
-    }
-  }
+  for (int i = 0; i < IF / 2; ++i)
+    n4[i] = *reinterpret_cast<const f32x4*>(st.N + wr * (BM / 2) + i * 16 + h * 4);
+#pragma unroll
+  for (int j = 0; j < CF; ++j) sc[j] = f16_to_f32((uint16_t)st.S[wc * (CF * 16) + j * 16 + lr]);
 }
 
 // Raw form: corrections -136 * sum_k x[m][k] of the group in stage st for
@@ -344,10 +395,15 @@ __device__ __forceinline__ void load_b(const Stage& st, int wave, int h, int lr,
 // holds the row's sum).
 __device__ __forceinline__ f32x4 row_corrections(const Stage& st, int wave, int h, int lr) {
   const int row = wave * 16 + lr;
+  bf16x8 x[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) x[s] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
+  // all four reads in flight before the chain starts
+  __builtin_amdgcn_sched_barrier(0);
   const bf16x8 neg = neg136x8();
   f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int s = 0; s < 4; ++s) c = mfma16x16x32(as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]), neg, c);
+  for (int s = 0; s < 4; ++s) c = mfma16x16x32(x[s], neg, c);
   return c;
 }
 
@@ -357,73 +413,106 @@ __device__ __forceinline__ void store_corrections(const Stage& st, int wave, int
   if (lr == 0) *reinterpret_cast<f32x4*>(st.N + wave * 16 + h * 4) = c;
 }
 
-// One group.  On entry bq holds the group's unpacked codes and (a, n4) its
-// row fragment 0; fragment i + 1 is read from LDS during fragment i's MFMAs.
-// The scale FMAs of fragment i are issued during fragment i + 1; those of
-// fragment 7 are carried in (cprev, sprev) into the next group.  Before the
-// last fragment every read of `cur` is complete, so the wave waits for its
-// copies of the next group and joins the step barrier; the next group's
-// codes and fragment 0 are then read from `nxt` under fragment 7's MFMAs.
-// Raw form: the wave's own copies of the next group land before fragment
-// IF - 2 (the wait moves there), the correction chain of its rows is issued
-// ahead of that fragment's MFMAs and stored after them, before the barrier.
-template <int IF, bool RAW>
-__device__ __forceinline__ void compute_stage(const Stage& cur, const Stage& nxt, int wave,
-                                              int lane, bf16x8 (&bq)[JF][4], bf16x8 (&a)[4],
-                                              f32x4& n4, f32x4 (&cprev)[JF], float (&sprev)[JF],
-                                              f32x4 (&acc)[IF][JF]) {
-  static_assert(!RAW || IF >= 2, "raw form needs two fragments per stage");
-  const int h = lane >> 4, lr = lane & 15;
-  float scf[JF];
-#pragma unroll
-  for (int j = 0; j < JF; ++j) scf[j] = f16_to_f32((uint16_t)cur.S[wave * WN + j * 16 + lr]);
-  bf16x8 an[4];
-  f32x4 nn, corr;
-#pragma unroll
-  for (int i = 0; i < IF; ++i) {
-    if (i + 1 < IF) {
-      load_a(cur, i + 1, h, lr, an, nn);
-      if (RAW && i == IF - 2) {
-        __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
-        corr = row_corrections(nxt, wave, h, lr);
-      }
-    } else {
+// State a wave carries from one group step to the next.
+template <int IF>
+struct Carry {
+  static constexpr int RF = IF / 2, NC = RF * CF, HALF = NC / 2;
+  f32x4 acc[RF][CF];   // scaled sums
+  f32x4 c[RF][CF];     // chains of the current group
+  bf16x8 a[RF];        // activations of the next phase
+  bf16x8 b[CF];        // unpacked codes of the next phase
+  u32x4 raw[CF];       // codes of the current group
+  f32x4 n4[RF];        // chain starts of the current group
+  f32x4 sc;            // scales of the current group (one per column fragment)
+  f32x4 sprev;         // scales of the previous group (its second-half chains)
+};
+
+// One 32-k phase S of group step g (see compute_step).
+template <int IF, bool RAW, int S>
+__device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt, int wave,
+                                              int lane, Carry<IF>& C) {
+  constexpr int RF = Carry<IF>::RF, NC = Carry<IF>::NC, HALF = Carry<IF>::HALF;
+  const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
+  bf16x8 an[RF];
+  if constexpr (S < 3) {
+    read_a<IF>(cur, wr, S + 1, h, lr, an);
+  } else {
+    __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
+    if constexpr (RAW) {
+      // chain starts of this wave's rows of group g + 1 (its own copies,
+      // landed), stored before the barrier
+      store_corrections(nxt, wave, h, lr, row_corrections(nxt, wave, h, lr));
       __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
-      wg_barrier();
-      load_a(nxt, 0, h, lr, an, nn);
     }
-    f32x4 c[JF];
-#pragma unroll
-    for (int j = 0; j < JF; ++j) c[j] = n4;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-#pragma unroll
-      for (int j = 0; j < JF; ++j) c[j] = mfma16x16x32(a[s], bq[j][s], c[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < JF; ++j) acc[(i + IF - 1) % IF][j] += cprev[j] * sprev[j];
-    if (i == IF - 1) load_b<RAW>(nxt, wave, h, lr, bq);
-    // the correction chain was issued ahead of this fragment's MFMAs
-    if (RAW && i == IF - 2) store_corrections(nxt, wave, h, lr, corr);
-#pragma unroll
-    for (int j = 0; j < JF; ++j) {
-      cprev[j] = c[j];
-      sprev[j] = scf[j];
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) a[s] = an[s];
-    n4 = nn;
-    // keep the row fragments in program order: hoisting later fragments'
-    // LDS reads above this point would only raise register pressure
-    __builtin_amdgcn_sched_barrier(0);
+    wg_barrier();
+    read_a<IF>(nxt, wr, 0, h, lr, an);
   }
+  if constexpr (S == 0) read_group_terms<IF>(cur, wr, wc, h, lr, C.n4, C.sc);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int i = k / CF, j = k % CF;
+    if (S == 0 && k >= HALF) {
+      C.acc[i][j] += C.c[i][j] * C.sprev[j];
+      pin(C.acc[i][j]);
+    }
+    C.c[i][j] = mfma16x16x32(C.a[i], C.b[j], S == 0 ? C.n4[i] : C.c[i][j]);
+  }
+  if constexpr (S == 3) {
+#pragma unroll
+    for (int k = 0; k < HALF; ++k) {
+      const int i = k / CF, j = k % CF;
+      C.acc[i][j] += C.c[i][j] * C.sc[j];
+      pin(C.acc[i][j]);
+    }
+    C.sprev = C.sc;
+    // the next group's codes (the current ones are dead after phase 2)
+    read_codes(nxt, wc, h, lr, C.raw);
+  }
+  // code words of the next phase
+#pragma unroll
+  for (int j = 0; j < CF; ++j) {
+    C.b[j] = unpack_word<RAW>(word<(S + 1) & 3>(C.raw[j]));
+    pin(C.b[j]);
+  }
+#pragma unroll
+  for (int i = 0; i < RF; ++i) C.a[i] = an[i];
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// One group step g from stage `cur`, in four 32-k phases.  Each phase runs
+// the 4 MFMAs of all RF x CF chains for one 32-k slice, reads the next
+// phase's activations from LDS at its top, and unpacks the next phase's code
+// words after its MFMAs, so unpacking is spread evenly over the step.  Chain
+// k's scale FMA (acc += chain * s) follows its last MFMA: for the first half
+// of the chains in phase 3, for the second half in phase 0 of the next step,
+// just before the chain is restarted.
+//
+// Before phase 3 every read of `cur` has been issued, so the wave waits for
+// its copies of group g + 1 and joins the step barrier; phase 3 then reads
+// group g + 1's first-phase activations and codes from `nxt` (its chain
+// starts and scales are read at the top of the next step).  The copies of
+// group g + 2 go into the third stage at the start of the step, so every
+// copy has about two steps to land.
+// Raw form: before the barrier each wave derives the chain starts of its 16
+// rows of group g + 1 (its own copies) and stores them.
+template <int IF, bool RAW>
+__device__ __forceinline__ void compute_step(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
+                                             int64_t m0, int g, const Stage& cur,
+                                             const Stage& nxt, const Stage& fut, int wave,
+                                             int lane, Carry<IF>& C) {
+  issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, p.G - 1), fut, wave, lane);
+  compute_phase<IF, RAW, 0>(cur, nxt, wave, lane, C);
+  compute_phase<IF, RAW, 1>(cur, nxt, wave, lane, C);
+  compute_phase<IF, RAW, 2>(cur, nxt, wave, lane, C);
+  compute_phase<IF, RAW, 3>(cur, nxt, wave, lane, C);
 }
 
 template <int EPI, bool PREP, int IF, bool RAW>
 __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   static_assert(!RAW || (IF == 8 && !PREP), "raw form: 128-row tiles, plain epilogues");
   using TM = TileM<IF>;
-  constexpr int BM = TM::BM;
+  constexpr int BM = TM::BM, RF = IF / 2;
   __shared__ u32x4 sA0[TM::A_SLOTS], sA1[TM::A_SLOTS], sA2[TM::A_SLOTS];
   __shared__ u32x4 sB0[B_SLOTS], sB1[B_SLOTS], sB2[B_SLOTS];
   __shared__ float sN0[TM::N_SLOTS], sN1[TM::N_SLOTS], sN2[TM::N_SLOTS];
@@ -432,6 +521,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, lr = lane & 15, h = lane >> 4;
+  const int wr = wave / WC, wc = wave % WC;
 
   // workgroup -> tile: first spread consecutive tiles over the 8 XCDs'
   // dispatch order so that each XCD sees a contiguous tile range, then walk
@@ -473,58 +563,54 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   const uint32_t os =
       (uint32_t)(min<int64_t>(n0 + ((wave - 2) & 3) * 64 + lane, p.N - 1) * p.G);
 
-  f32x4 acc[IF][JF];
+  Carry<IF> C;
 #pragma unroll
-  for (int i = 0; i < IF; ++i)
+  for (int i = 0; i < RF; ++i)
 #pragma unroll
-    for (int j = 0; j < JF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < CF; ++j) {
+      C.acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      C.c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};  // the first step's deferred FMAs add 0 * 0
+    }
+  C.sprev = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // group g lives in stage g % 3; step g issues group g + 2, clamped to the
-  // last group so that every step issues the same copies (the surplus ones
-  // land in a stage that is not read again)
-  const int G = p.G, Gl = p.G - 1;
+  // group g lives in stage g % 3; step g issues group g + 2 (clamped to the
+  // last group, so every step issues the same copies; the surplus ones land
+  // in a stage that is not read again)
+  const int G = p.G;
   issue_stage<IF, RAW>(p, o, os, m0, 0, S0, wave, lane);
-  issue_stage<IF, RAW>(p, o, os, m0, min(1, Gl), S1, wave, lane);
+  issue_stage<IF, RAW>(p, o, os, m0, min(1, G - 1), S1, wave, lane);
   __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   if constexpr (RAW) {
     store_corrections(S0, wave, h, lr, row_corrections(S0, wave, h, lr));
     __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   }
   wg_barrier();
-
-  bf16x8 bq[JF][4], a[4];
-  f32x4 n4;
-  f32x4 cprev[JF];  // carried chain of the last fragment; starts as 0 * 0
-  float sprev[JF];
+  read_a<IF>(S0, wr, 0, h, lr, C.a);
+  read_codes(S0, wc, h, lr, C.raw);
 #pragma unroll
-  for (int j = 0; j < JF; ++j) {
-    cprev[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    sprev[j] = 0.f;
-  }
-  load_b<RAW>(S0, wave, h, lr, bq);
-  load_a(S0, 0, h, lr, a, n4);
+  for (int j = 0; j < CF; ++j) C.b[j] = unpack_word<RAW>(C.raw[j].x);
+
   int g = 0;
   for (;;) {
-    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S2, wave, lane);
-    compute_stage<IF, RAW>(S0, S1, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_step<IF, RAW>(p, o, os, m0, g, S0, S1, S2, wave, lane, C);
     if (++g >= G) break;
-    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S0, wave, lane);
-    compute_stage<IF, RAW>(S1, S2, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_step<IF, RAW>(p, o, os, m0, g, S1, S2, S0, wave, lane, C);
     if (++g >= G) break;
-    issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, Gl), S1, wave, lane);
-    compute_stage<IF, RAW>(S2, S0, wave, lane, bq, a, n4, cprev, sprev, acc);
+    compute_step<IF, RAW>(p, o, os, m0, g, S2, S0, S1, wave, lane, C);
     if (++g >= G) break;
   }
   // no copy may still be writing LDS when the workgroup retires
   __builtin_amdgcn_s_waitcnt(0);
+  // the last group's second-half chains
 #pragma unroll
-  for (int j = 0; j < JF; ++j) acc[IF - 1][j] += cprev[j] * sprev[j];
+  for (int k = Carry<IF>::HALF; k < Carry<IF>::NC; ++k)
+    C.acc[k / CF][k % CF] += C.c[k / CF][k % CF] * C.sprev[k % CF];
 
   if constexpr (PREP) {
-    __shared__ float part[NW * BM];
-    store_tile<EPI, true, IF>(p, m0, n0, wave, lane, acc, part);
+    __shared__ float part[WC * BM];
+    store_tile<EPI, true, IF>(p, m0, n0, wave, lane, C.acc, part);
   } else {
-    store_tile<EPI, false, IF>(p, m0, n0, wave, lane, acc, nullptr);
+    store_tile<EPI, false, IF>(p, m0, n0, wave, lane, C.acc, nullptr);
   }
 }
 
