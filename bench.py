@@ -74,6 +74,48 @@ def measured_traffic(kernel_symbol: str):
     return int(k["bytes_per_launch"])
 
 
+class ClockSampler:
+    """Samples the GPU's current graphics clock (amdsmi, every ~20 ms) on a
+    host thread while the timed region runs; mean() is the average in GHz,
+    or None when the clock cannot be read."""
+
+    def __init__(self, interval=0.02):
+        import threading
+
+        self.interval, self.samples, self._stop = interval, [], threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        try:
+            import amdsmi
+
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+        except Exception:
+            self._smi = None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                info = self._smi.amdsmi_get_clock_info(self._h, self._smi.AmdSmiClkType.GFX)
+                self.samples.append(float(info["clk"]))
+            except Exception:
+                pass
+            self._stop.wait(self.interval)
+
+    def __enter__(self):
+        if self._smi is not None:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._smi is not None:
+            self._thread.join()
+
+    def mean(self):
+        return round(sum(self.samples) / len(self.samples) / 1000.0, 3) if self.samples else None
+
+
 def build_stack(ql, synth, torch, L, d, dff):
     shapes = {"qkv": (3 * d, d), "out": (d, d), "up": (dff, d), "down": (d, dff)}
     scratch = torch.empty(dff * d, dtype=torch.float32, device="cuda")
@@ -123,12 +165,14 @@ def bench_stack(args, ql, synth, torch):
         for e in ev:
             e.record()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(evs[k])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    with ClockSampler() as clk:
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step(evs[k])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
+    clock_ghz = clk.mean()
 
     flops = {"qkv": 2 * M * d * 3 * d, "out": 2 * M * d * d, "up": 2 * M * d * dff,
              "down": 2 * M * dff * d}
@@ -172,6 +216,12 @@ def bench_stack(args, ql, synth, torch):
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "flops_per_launch": int(ff / nn), "launches": nn,
+                     # the same fraction against the peak at the clock the
+                     # chip actually ran during the timed steps (the datasheet
+                     # peak assumes 2.4 GHz)
+                     "clock_GHz_measured": clock_ghz,
+                     "frac_at_measured_clock": (round(achieved / (PEAK_BF16_TFLOPS * clock_ghz / 2.4),
+                                                      4) if clock_ghz else None),
                      "traffic": measured_traffic(SYMBOL[sym]), "traffic_unit": "bytes/launch"},
         "kernels": kern,
         "gemm_share_of_step": round(gemm_ms / ms, 4),
