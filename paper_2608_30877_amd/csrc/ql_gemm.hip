@@ -433,7 +433,8 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
                                               int lane, Carry<IF>& C) {
   constexpr int RF = Carry<IF>::RF, NC = Carry<IF>::NC, HALF = Carry<IF>::HALF;
   const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
-  bf16x8 an[RF];
+  bf16x8 an[RF], nb[CF];
+  u32x4 rawn[CF];
   if constexpr (S < 3) {
     read_a<IF>(cur, wr, S + 1, h, lr, an);
   } else {
@@ -449,6 +450,17 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
   }
   if constexpr (S == 0) read_group_terms<IF>(cur, wr, wc, h, lr, C.n4, C.sc);
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (S == 3) read_codes(nxt, wc, h, lr, rawn);
+  // The phase's MFMAs one by one, each followed by its share of the VALU
+  // work and a scheduling barrier, so that every wave interleaves its MFMAs
+  // and VALU evenly: the other wave on the SIMD then finds the matrix core
+  // or the VALU free, instead of both waves contending for the same one.
+  //   * phase 0: before chain k's first MFMA (k >= HALF), the deferred
+  //     scale FMA of the previous group's chain k;
+  //   * phase 3: after the MFMA of chain k >= HALF, the scale FMA of chain
+  //     k - HALF (its last MFMA issued HALF MFMAs earlier);
+  //   * every NC / CF MFMAs: one code word of the next phase unpacked.
+  constexpr int PER_WORD = NC / CF;
 #pragma unroll
   for (int k = 0; k < NC; ++k) {
     const int i = k / CF, j = k % CF;
@@ -457,24 +469,26 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
       pin(C.acc[i][j]);
     }
     C.c[i][j] = mfma16x16x32(C.a[i], C.b[j], S == 0 ? C.n4[i] : C.c[i][j]);
+    if (S == 3 && k >= HALF) {
+      const int i2 = (k - HALF) / CF, j2 = (k - HALF) % CF;
+      C.acc[i2][j2] += C.c[i2][j2] * C.sc[j2];
+      pin(C.acc[i2][j2]);
+    }
+    if (k % PER_WORD == PER_WORD - 1) {
+      const int jw = k / PER_WORD;
+      // code word of the next phase (the next group's first word in phase 3)
+      nb[jw] = unpack_word<RAW>(word<(S + 1) & 3>(S < 3 ? C.raw[jw] : rawn[jw]));
+      pin(nb[jw]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
   if constexpr (S == 3) {
-#pragma unroll
-    for (int k = 0; k < HALF; ++k) {
-      const int i = k / CF, j = k % CF;
-      C.acc[i][j] += C.c[i][j] * C.sc[j];
-      pin(C.acc[i][j]);
-    }
     C.sprev = C.sc;
-    // the next group's codes (the current ones are dead after phase 2)
-    read_codes(nxt, wc, h, lr, C.raw);
-  }
-  // code words of the next phase
 #pragma unroll
-  for (int j = 0; j < CF; ++j) {
-    C.b[j] = unpack_word<RAW>(word<(S + 1) & 3>(C.raw[j]));
-    pin(C.b[j]);
+    for (int j = 0; j < CF; ++j) C.raw[j] = rawn[j];
   }
+#pragma unroll
+  for (int j = 0; j < CF; ++j) C.b[j] = nb[j];
 #pragma unroll
   for (int i = 0; i < RF; ++i) C.a[i] = an[i];
   __builtin_amdgcn_sched_barrier(0);
