@@ -30,6 +30,8 @@
 // call needs no staging buffer at all.
 #include <algorithm>
 
+#include <type_traits>
+
 #include "ql_device.h"
 #include "ql_internal.h"
 
@@ -53,9 +55,10 @@ struct TileM {
   static constexpr int A_SLOTS = BM * 16;             // 16-byte slots per stage
   static constexpr int A_PER_WAVE = A_SLOTS / 64 / NW;
   static constexpr int N_SLOTS = BM < 64 ? 64 : BM;   // correction terms (+ clamped copies)
-  // Copies each wave issues per group after its single correction / scale
-  // copy (see issue_stage); waiting until at most this many are outstanding
-  // means every copy of the group before has landed.
+  // Activation and code copies each wave issues per group, after its
+  // correction / scale copy if it has one (see issue_copy); once the next
+  // group's copies are all issued, waiting until at most this many are
+  // outstanding means every copy of the group before has landed.
   static constexpr int kLaterCopies = A_PER_WAVE + B_PER_WAVE;
   static_assert(kLaterCopies < 16, "vmcnt immediate");
   // s_waitcnt immediate (gfx9 layout): vmcnt(kLaterCopies), lgkmcnt(0),
@@ -77,6 +80,9 @@ struct GemmParams {
   float* pns;
   int64_t pld;
   int pcol0;
+  // 1: the scales are copied eight groups at a time (16 bytes per column;
+  // needs G % 8 == 0 and a 16-byte aligned sc)
+  int sbatch;
 };
 
 template <int CTRL>
@@ -89,17 +95,24 @@ __device__ __forceinline__ float dpp_f32(float v) {
 // (x0,x4,x1,x5,x2,x6,x3,x7)
 __device__ __forceinline__ int perm8(int e) { return 2 * (e & 3) + (e >> 2); }
 
-// LDS slot swizzles.  gfx950 serves a 16-byte-per-lane LDS read in four
-// cycles; one cycle takes the 4-lane quads of a half-wave whose quad index
-// (lane bits 2-4) has a given parity, so a pattern is conflict-free when each
-// such set of 16 lanes covers all 16 slots of a 256-byte bank row.  Row r of
-// the activation tile stores logical 16-byte chunk c at slot c ^ a_msk(r);
-// column n of the weight tile stores its 16-byte piece h at slot h ^ b_swz(n).
-__device__ __forceinline__ int a_msk(int row) {
-  row &= 15;
-  return row ^ ((((row >> 2) ^ (row >> 3)) & 1) << 2);
+// LDS layouts.  gfx950 serves a 16-byte-per-lane LDS read in four cycles; one
+// cycle takes the 4-lane quads of a half-wave whose quad index (lane bits
+// 2-4) has a given parity, so a pattern is conflict-free when each such set
+// of 16 lanes covers all 16 slots of a 256-byte bank row.
+//
+// Activation tile: 1 KB blocks of 4 rows (64 16-byte slots; one copy fills
+// one block from 4 whole 256-byte row segments).  Inside a block, phase s
+// (16 slots) comes first, then row r % 4 (4 slots), then the k-quarter h
+// (16-byte chunk 4h + s of the row's group), swizzled by bit 3 of the row.
+// A fragment read (16 rows, one phase) by lane (h, lr) then differs between
+// phases and row fragments only by a constant, and each 16-lane set -- rows
+// r % 4 = 0..3 twice, once with bit 3 clear and once set, and two values of
+// h -- covers all 16 slots.
+__device__ __forceinline__ int a_swz(int row) { return ((row >> 3) & 1) << 1; }
+__device__ __forceinline__ int a_slot(int row, int s, int h) {
+  return (row >> 2) * 64 + s * 16 + (row & 3) * 4 + (h ^ a_swz(row));
 }
-__device__ __forceinline__ int a_phys(int row, int chunk) { return chunk ^ a_msk(row); }
+// Code tile: column n stores its 16-byte piece h at slot 4n + (h ^ b_swz(n)).
 __device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2)) & 3; }
 
 // Direct-to-LDS copies: lane l writes lds + l * BYTES (a 2-byte copy writes
@@ -135,44 +148,12 @@ __device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, cons
   }
 }
 
-// NA 16-byte activation copies (base xa) then two 16-byte code copies (base
-// qb), in one sequence
-template <int NA>
-__device__ __forceinline__ void copy16_to_lds(const void* xa, const uint32_t (&oa)[NA],
-                                              const uint32_t (&la)[NA], const void* qb,
-                                              uint32_t ob0, uint32_t lb0, uint32_t ob1,
-                                              uint32_t lb1) {
+// one 16-byte copy (activations, codes)
+__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds) {
   uint32_t saved;
-#define QL_X16 "global_load_lds_dwordx4"
-  if constexpr (NA == 1) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
-                 QL_LDS_COPY(QL_X16, "b0", "qb", "m0v") QL_LDS_COPY(QL_X16, "b1", "qb", "m1v")
-                 "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved)
-                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [b0] "v"(ob0),
-                   [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
-                 : "memory");
-  } else if constexpr (NA == 2) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
-                 QL_LDS_COPY(QL_X16, "a1", "xa", "l1") QL_LDS_COPY(QL_X16, "b0", "qb", "m0v")
-                 QL_LDS_COPY(QL_X16, "b1", "qb", "m1v") "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved)
-                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [a1] "v"(oa[1]),
-                   [l1] "s"(la[1]), [b0] "v"(ob0), [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
-                 : "memory");
-  } else {
-    static_assert(NA == 4, "activation copies per wave");
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY(QL_X16, "a0", "xa", "l0")
-                 QL_LDS_COPY(QL_X16, "a1", "xa", "l1") QL_LDS_COPY(QL_X16, "a2", "xa", "l2")
-                 QL_LDS_COPY(QL_X16, "a3", "xa", "l3") QL_LDS_COPY(QL_X16, "b0", "qb", "m0v")
-                 QL_LDS_COPY(QL_X16, "b1", "qb", "m1v") "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved)
-                 : [xa] "s"(xa), [qb] "s"(qb), [a0] "v"(oa[0]), [l0] "s"(la[0]), [a1] "v"(oa[1]),
-                   [l1] "s"(la[1]), [a2] "v"(oa[2]), [l2] "s"(la[2]), [a3] "v"(oa[3]),
-                   [l3] "s"(la[3]), [b0] "v"(ob0), [m0v] "s"(lb0), [b1] "v"(ob1), [m1v] "s"(lb1)
-                 : "memory");
-  }
-#undef QL_X16
+  asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dwordx4", "o", "b", "l")
+               "s_mov_b32 m0, %[sv]"
+               : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(lds) : "memory");
 }
 #undef QL_LDS_COPY
 
@@ -220,29 +201,84 @@ __device__ __forceinline__ int a_block(int j, int wave) {
   return RAW ? wave * TileM<IF>::A_PER_WAVE + j : j * NW + wave;
 }
 
-// Copies of group g into stage st.  Prepared form: waves 0-1 copy the BM
-// correction terms (rows past BM repeat the last one); both forms: waves 2-5
-// copy the 256 scales; then every wave issues its activation and code copies.
+// The copies of group g into stage st, as seen by one wave.
+template <int IF>
+struct CopyJob {
+  const GemmParams& p;
+  const Offsets<IF>& o;
+  uint32_t os;
+  int64_t m0;
+  int g;
+  Stage st;
+  uint16_t* sb;  // the two eight-group scale buffers ([2][BN][8])
+  int wave, lane;
+};
+
+// Copy J of a wave's NCOPY copies of a group (J is a compile-time index).
+// J = 0: prepared form, waves 0-1 copy the BM correction terms (rows past BM
+// repeat the last one); both forms, waves 2-5 copy the 256 scales.  J = 1 ..
+// A_PER_WAVE: the wave's activation copies; the last two: its code copies.
+template <int IF>
+constexpr int kCopies = TileM<IF>::A_PER_WAVE + B_PER_WAVE + 1;
+
+template <int IF, bool RAW, int J>
+__device__ __forceinline__ void issue_copy(const CopyJob<IF>& c) {
+  constexpr int BM = TileM<IF>::BM, NA = TileM<IF>::A_PER_WAVE;
+  static_assert(B_PER_WAVE == 2 && J < kCopies<IF>, "copy index");
+  const int wave = c.wave;
+  if constexpr (J == 0) {
+    if (!RAW && wave * 64 < BM)
+      copy_to_lds<4>(c.p.ns + (size_t)c.g * c.p.Mp + c.m0,
+                     (uint32_t)min(wave * 64 + c.lane, BM - 1) * 4, c.st.N + wave * 64);
+    else if (wave >= 2 && wave < 6) {
+      if (c.p.sbatch) {
+        // groups g .. g + 7 of 64 columns, 16 bytes per column, into the
+        // buffer of batch g / 8 (read from step g on; the buffer's previous
+        // batch was last read eight steps earlier)
+        if ((c.g & 7) == 0)
+          copy16_to_lds(c.p.sc + c.g, c.os * 2,
+                        (uint32_t)reinterpret_cast<uintptr_t>(
+                            c.sb + ((c.g >> 3) & 1) * (BN * 8) + (wave - 2) * 64 * 8));
+      } else {
+        copy_to_lds<2>(c.p.sc + c.g, c.os * 2, c.st.S + (wave - 2) * 64);
+      }
+    }
+  } else if constexpr (J <= NA) {
+    const char* xa = reinterpret_cast<const char*>(c.p.xp) + (size_t)c.g * (kGroup * 2);
+    copy16_to_lds(xa, c.o.a[J - 1],
+                  (uint32_t)reinterpret_cast<uintptr_t>(c.st.A + a_block<IF, RAW>(J - 1, wave) * 64));
+  } else {
+    const char* qb = reinterpret_cast<const char*>(c.p.qw) + (size_t)c.g * (kGroup / 2);
+    copy16_to_lds(qb, c.o.b[J - NA - 1],
+                  (uint32_t)reinterpret_cast<uintptr_t>(c.st.B + ((J - NA - 1) * NW + wave) * 64));
+  }
+}
+
+template <int J, int N, class F>
+__device__ __forceinline__ void static_for(const F& f) {
+  if constexpr (J < N) {
+    f(std::integral_constant<int, J>{});
+    static_for<J + 1, N>(f);
+  }
+}
+
+// all copies of a group at once (the two groups before the loop)
 template <int IF, bool RAW>
-__device__ __forceinline__ void issue_stage(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
-                                            int64_t m0, int g, const Stage& st, int wave, int lane) {
-  constexpr int BM = TileM<IF>::BM;
-  const char* xa = reinterpret_cast<const char*>(p.xp) + (size_t)g * (kGroup * 2);
-  const char* qb = reinterpret_cast<const char*>(p.qw) + (size_t)g * (kGroup / 2);
-  if (!RAW && wave * 64 < BM)
-    copy_to_lds<4>(p.ns + (size_t)g * p.Mp + m0, (uint32_t)min(wave * 64 + lane, BM - 1) * 4,
-                   st.N + wave * 64);
-  else if (wave >= 2 && wave < 6)
-    copy_to_lds<2>(p.sc + g, os * 2, st.S + (wave - 2) * 64);
-  constexpr int NA = TileM<IF>::A_PER_WAVE;
-  static_assert(B_PER_WAVE == 2, "two code copies per wave");
-  uint32_t alds[NA];
-#pragma unroll
-  for (int j = 0; j < NA; ++j)
-    alds[j] = (uint32_t)reinterpret_cast<uintptr_t>(st.A + a_block<IF, RAW>(j, wave) * 64);
-  copy16_to_lds<NA>(xa, o.a, alds, qb, o.b[0],
-                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (0 * NW + wave) * 64), o.b[1],
-                    (uint32_t)reinterpret_cast<uintptr_t>(st.B + (1 * NW + wave) * 64));
+__device__ __forceinline__ void issue_stage(const CopyJob<IF>& c) {
+  static_for<0, kCopies<IF>>([&](auto J) { issue_copy<IF, RAW, decltype(J)::value>(c); });
+}
+
+// In the loop, copy J is issued after MFMA slot J * 2 NC / NCOPY of the first
+// two phases (NC MFMAs per phase), not in one burst: a burst of 56 16-byte
+// copies per workgroup at the top of every step fills the address unit's
+// queue, and the waves stall on it in front of their MFMAs.
+template <int IF, bool RAW>
+__device__ __forceinline__ void issue_copies_at(const CopyJob<IF>& c, int slot) {
+  constexpr int NC = (IF / 2) * 4;
+  static_for<0, kCopies<IF>>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    if (slot == j * 2 * NC / kCopies<IF>) issue_copy<IF, RAW, j>(c);
+  });
 }
 
 // Wave layout: the 8 waves form a 2 x 4 grid over the 128 x 256 tile; wave
@@ -345,7 +381,7 @@ __device__ __forceinline__ void read_a(const Stage& st, int wr, int s, int h, in
 #pragma unroll
   for (int i = 0; i < IF / 2; ++i) {
     const int row = wr * (BM / 2) + i * 16 + lr;
-    a[i] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
+    a[i] = as_bf16x8(st.A[a_slot(row, s, h)]);
   }
 }
 
@@ -377,16 +413,28 @@ __device__ __forceinline__ uint32_t word(const u32x4& v) {
 }
 
 // corrections (chain starts) and scales of a group for the wave's fragments
+// chain starts (the groups' correction terms) of the wave's row fragments
 template <int IF>
-__device__ __forceinline__ void read_group_terms(const Stage& st, int wr, int wc, int h, int lr,
-                                                 f32x4 (&n4)[IF / 2], f32x4& sc) {
-  static_assert(CF == 4, "one scale per vector element");
+__device__ __forceinline__ void read_chain_starts(const Stage& st, int wr, int h,
+                                                  f32x4 (&n4)[IF / 2]) {
   constexpr int BM = TileM<IF>::BM;
 #pragma unroll
   for (int i = 0; i < IF / 2; ++i)
     n4[i] = *reinterpret_cast<const f32x4*>(st.N + wr * (BM / 2) + i * 16 + h * 4);
+}
+
+// binary16 scales of group g for the wave's column fragments, kept as bits
+// (converted where they are used, so that no instruction waits on the read)
+__device__ __forceinline__ void read_scales(const Stage& st, const uint16_t* sb, int g,
+                                            bool sbatch, int wc, int lr, uint32_t (&sc)[CF]) {
+  if (sbatch) {
+    const uint16_t* b = sb + ((g >> 3) & 1) * (BN * 8) + (g & 7);
 #pragma unroll
-  for (int j = 0; j < CF; ++j) sc[j] = f16_to_f32((uint16_t)st.S[wc * (CF * 16) + j * 16 + lr]);
+    for (int j = 0; j < CF; ++j) sc[j] = b[(wc * (CF * 16) + j * 16 + lr) * 8];
+  } else {
+#pragma unroll
+    for (int j = 0; j < CF; ++j) sc[j] = st.S[wc * (CF * 16) + j * 16 + lr];
+  }
 }
 
 // Raw form: corrections -136 * sum_k x[m][k] of the group in stage st for
@@ -397,7 +445,7 @@ __device__ __forceinline__ f32x4 row_corrections(const Stage& st, int wave, int 
   const int row = wave * 16 + lr;
   bf16x8 x[4];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) x[s] = as_bf16x8(st.A[row * 16 + a_phys(row, h * 4 + s)]);
+  for (int s = 0; s < 4; ++s) x[s] = as_bf16x8(st.A[a_slot(row, s, h)]);
   // all four reads in flight before the chain starts
   __builtin_amdgcn_sched_barrier(0);
   const bf16x8 neg = neg136x8();
@@ -423,14 +471,15 @@ struct Carry {
   bf16x8 b[CF];        // unpacked codes of the next phase
   u32x4 raw[CF];       // codes of the current group
   f32x4 n4[RF];        // chain starts of the current group
-  f32x4 sc;            // scales of the current group (one per column fragment)
-  f32x4 sprev;         // scales of the previous group (its second-half chains)
+  uint32_t sc[CF];     // binary16 scales of the current group, one per column fragment
+  uint32_t sprev[CF];  // those of the previous group (its second-half chains)
 };
 
 // One 32-k phase S of group step g (see compute_step).
 template <int IF, bool RAW, int S>
-__device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt, int wave,
-                                              int lane, Carry<IF>& C) {
+__device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt,
+                                              const CopyJob<IF>& cj, int g, int wave, int lane,
+                                              Carry<IF>& C) {
   constexpr int RF = Carry<IF>::RF, NC = Carry<IF>::NC, HALF = Carry<IF>::HALF;
   const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
   bf16x8 an[RF], nb[CF];
@@ -446,11 +495,14 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
       __builtin_amdgcn_s_waitcnt(TileM<IF>::kWaitPrevGroup);
     }
     wg_barrier();
+    // the codes (unpacked from the fourth MFMA on) and the chain starts (the
+    // next step's first MFMAs) before the activations (its second phase)
+    read_codes(nxt, wc, h, lr, rawn);
+    read_chain_starts<IF>(nxt, wr, h, C.n4);
     read_a<IF>(nxt, wr, 0, h, lr, an);
   }
-  if constexpr (S == 0) read_group_terms<IF>(cur, wr, wc, h, lr, C.n4, C.sc);
+  if constexpr (S == 0) read_scales(cur, cj.sb, g, cj.p.sbatch != 0, wc, lr, C.sc);
   __builtin_amdgcn_sched_barrier(0);
-  if constexpr (S == 3) read_codes(nxt, wc, h, lr, rawn);
   // The phase's MFMAs one by one, each followed by its share of the VALU
   // work and a scheduling barrier, so that every wave interleaves its MFMAs
   // and VALU evenly: the other wave on the SIMD then finds the matrix core
@@ -465,13 +517,13 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
   for (int k = 0; k < NC; ++k) {
     const int i = k / CF, j = k % CF;
     if (S == 0 && k >= HALF) {
-      C.acc[i][j] += C.c[i][j] * C.sprev[j];
+      C.acc[i][j] += C.c[i][j] * f16_to_f32((uint16_t)C.sprev[j]);
       pin(C.acc[i][j]);
     }
     C.c[i][j] = mfma16x16x32(C.a[i], C.b[j], S == 0 ? C.n4[i] : C.c[i][j]);
     if (S == 3 && k >= HALF) {
       const int i2 = (k - HALF) / CF, j2 = (k - HALF) % CF;
-      C.acc[i2][j2] += C.c[i2][j2] * C.sc[j2];
+      C.acc[i2][j2] += C.c[i2][j2] * f16_to_f32((uint16_t)C.sc[j2]);
       pin(C.acc[i2][j2]);
     }
     if (k % PER_WORD == PER_WORD - 1) {
@@ -480,10 +532,12 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
       nb[jw] = unpack_word<RAW>(word<(S + 1) & 3>(S < 3 ? C.raw[jw] : rawn[jw]));
       pin(nb[jw]);
     }
+    if constexpr (S < 2) issue_copies_at<IF, RAW>(cj, S * NC + k);
     __builtin_amdgcn_sched_barrier(0);
   }
   if constexpr (S == 3) {
-    C.sprev = C.sc;
+#pragma unroll
+    for (int j = 0; j < CF; ++j) C.sprev[j] = C.sc[j];
 #pragma unroll
     for (int j = 0; j < CF; ++j) C.raw[j] = rawn[j];
   }
@@ -506,20 +560,20 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
 // its copies of group g + 1 and joins the step barrier; phase 3 then reads
 // group g + 1's first-phase activations and codes from `nxt` (its chain
 // starts and scales are read at the top of the next step).  The copies of
-// group g + 2 go into the third stage at the start of the step, so every
-// copy has about two steps to land.
+// group g + 2 go into the third stage during the first two phases of the
+// step, so every copy has about two steps to land.
 // Raw form: before the barrier each wave derives the chain starts of its 16
 // rows of group g + 1 (its own copies) and stores them.
 template <int IF, bool RAW>
 __device__ __forceinline__ void compute_step(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
                                              int64_t m0, int g, const Stage& cur,
-                                             const Stage& nxt, const Stage& fut, int wave,
-                                             int lane, Carry<IF>& C) {
-  issue_stage<IF, RAW>(p, o, os, m0, min(g + 2, p.G - 1), fut, wave, lane);
-  compute_phase<IF, RAW, 0>(cur, nxt, wave, lane, C);
-  compute_phase<IF, RAW, 1>(cur, nxt, wave, lane, C);
-  compute_phase<IF, RAW, 2>(cur, nxt, wave, lane, C);
-  compute_phase<IF, RAW, 3>(cur, nxt, wave, lane, C);
+                                             const Stage& nxt, const Stage& fut, uint16_t* sb,
+                                             int wave, int lane, Carry<IF>& C) {
+  const CopyJob<IF> cj{p, o, os, m0, min(g + 2, p.G - 1), fut, sb, wave, lane};
+  compute_phase<IF, RAW, 0>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 1>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 2>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 3>(cur, nxt, cj, g, wave, lane, C);
 }
 
 template <int EPI, bool PREP, int IF, bool RAW>
@@ -527,11 +581,15 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   static_assert(!RAW || (IF == 8 && !PREP), "raw form: 128-row tiles, plain epilogues");
   using TM = TileM<IF>;
   constexpr int BM = TM::BM, RF = IF / 2;
-  __shared__ u32x4 sA0[TM::A_SLOTS], sA1[TM::A_SLOTS], sA2[TM::A_SLOTS];
-  __shared__ u32x4 sB0[B_SLOTS], sB1[B_SLOTS], sB2[B_SLOTS];
-  __shared__ float sN0[TM::N_SLOTS], sN1[TM::N_SLOTS], sN2[TM::N_SLOTS];
-  __shared__ uint32_t sS0[BN], sS1[BN], sS2[BN];
-  const Stage S0{sA0, sB0, sN0, sS0}, S1{sA1, sB1, sN1, sS1}, S2{sA2, sB2, sN2, sS2};
+  // each kind of tile of the three stages contiguous, so that one address
+  // register with constant offsets reaches the same slot in every stage
+  __shared__ u32x4 sA[3][TM::A_SLOTS];
+  __shared__ u32x4 sB[3][B_SLOTS];
+  __shared__ float sN[3][TM::N_SLOTS];
+  __shared__ uint32_t sS[3][BN];
+  const Stage S0{sA[0], sB[0], sN[0], sS[0]}, S1{sA[1], sB[1], sN[1], sS[1]},
+      S2{sA[2], sB[2], sN[2], sS[2]};
+  __shared__ __attribute__((aligned(16))) uint16_t sSB[2 * BN * 8];
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, lr = lane & 15, h = lane >> 4;
@@ -559,9 +617,10 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   Offsets<IF> o;
 #pragma unroll
   for (int j = 0; j < TM::A_PER_WAVE; ++j) {
-    const int slot = a_block<IF, RAW>(j, wave) * 64 + lane;
-    const int row = slot >> 4;
-    const int chunk = (slot & 15) ^ a_msk(row);
+    // lane l fills slot l of block a_block: phase l / 16, row l / 4 % 4 of
+    // the block, swizzled k-quarter l % 4
+    const int row = a_block<IF, RAW>(j, wave) * 4 + ((lane >> 2) & 3);
+    const int chunk = ((lane & 3) ^ a_swz(row)) * 4 + (lane >> 4);
     const int64_t r = min<int64_t>(m0 + row, p.M - 1);
     o.a[j] = (uint32_t)((r * (RAW ? p.ldx : (int64_t)p.K) + chunk * 8) * 2);
   }
@@ -585,40 +644,60 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
       C.acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
       C.c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};  // the first step's deferred FMAs add 0 * 0
     }
-  C.sprev = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < CF; ++j) C.sprev[j] = 0;
 
   // group g lives in stage g % 3; step g issues group g + 2 (clamped to the
   // last group, so every step issues the same copies; the surplus ones land
   // in a stage that is not read again)
   const int G = p.G;
-  issue_stage<IF, RAW>(p, o, os, m0, 0, S0, wave, lane);
-  issue_stage<IF, RAW>(p, o, os, m0, min(1, G - 1), S1, wave, lane);
+  issue_stage<IF, RAW>(CopyJob<IF>{p, o, os, m0, 0, S0, sSB, wave, lane});
+  issue_stage<IF, RAW>(CopyJob<IF>{p, o, os, m0, min(1, G - 1), S1, sSB, wave, lane});
   __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   if constexpr (RAW) {
     store_corrections(S0, wave, h, lr, row_corrections(S0, wave, h, lr));
     __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   }
   wg_barrier();
-  read_a<IF>(S0, wr, 0, h, lr, C.a);
   read_codes(S0, wc, h, lr, C.raw);
+  read_chain_starts<IF>(S0, wr, h, C.n4);
+  read_a<IF>(S0, wr, 0, h, lr, C.a);
 #pragma unroll
   for (int j = 0; j < CF; ++j) C.b[j] = unpack_word<RAW>(C.raw[j].x);
 
-  int g = 0;
-  for (;;) {
-    compute_step<IF, RAW>(p, o, os, m0, g, S0, S1, S2, wave, lane, C);
-    if (++g >= G) break;
-    compute_step<IF, RAW>(p, o, os, m0, g, S1, S2, S0, wave, lane, C);
-    if (++g >= G) break;
-    compute_step<IF, RAW>(p, o, os, m0, g, S2, S0, S1, wave, lane, C);
-    if (++g >= G) break;
+  if constexpr (RAW) {
+    // the raw form holds more registers in its step (the chain starts it
+    // derives); rotating the stages at run time, with scalar stage indices,
+    // keeps one address register per LDS access pattern instead of one per
+    // stage, and the loop free of spills
+    const auto stage = [&](int t) { return Stage{sA[t], sB[t], sN[t], sS[t]}; };
+    int cur = 0, nxt = 1, fut = 2;
+#pragma nounroll
+    for (int g = 0; g < G; ++g) {
+      compute_step<IF, RAW>(p, o, os, m0, g, stage(cur), stage(nxt), stage(fut), sSB, wave,
+                            lane, C);
+      const int t = cur;
+      cur = nxt;
+      nxt = fut;
+      fut = t;
+    }
+  } else {
+    int g = 0;
+    for (;;) {
+      compute_step<IF, RAW>(p, o, os, m0, g, S0, S1, S2, sSB, wave, lane, C);
+      if (++g >= G) break;
+      compute_step<IF, RAW>(p, o, os, m0, g, S1, S2, S0, sSB, wave, lane, C);
+      if (++g >= G) break;
+      compute_step<IF, RAW>(p, o, os, m0, g, S2, S0, S1, sSB, wave, lane, C);
+      if (++g >= G) break;
+    }
   }
   // no copy may still be writing LDS when the workgroup retires
   __builtin_amdgcn_s_waitcnt(0);
   // the last group's second-half chains
 #pragma unroll
   for (int k = Carry<IF>::HALF; k < Carry<IF>::NC; ++k)
-    C.acc[k / CF][k % CF] += C.c[k / CF][k % CF] * C.sprev[k % CF];
+    C.acc[k / CF][k % CF] += C.c[k / CF][k % CF] * f16_to_f32((uint16_t)C.sprev[k % CF]);
 
   if constexpr (PREP) {
     __shared__ float part[WC * BM];
@@ -667,6 +746,7 @@ GemmParams chunk_params(const uint16_t* x, int64_t ldx, const float* ns, int64_t
   p.pns = nullptr;
   p.pld = 0;
   p.pcol0 = 0;
+  p.sbatch = (p.G % 8 == 0 && reinterpret_cast<uintptr_t>(p.sc) % 16 == 0) ? 1 : 0;
   return p;
 }
 

@@ -105,6 +105,9 @@ SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel (32-, 64- and 128-row t
     (1, 64, 128), (5, 250, 384), (8, 512, 512), (16, 512, 512), (16, 1000, 1280),
     (17, 256, 256), (32, 256, 384), (48, 300, 256), (64, 384, 512), (128, 256, 512),
     (200, 500, 640), (300, 1024, 1152),
+    # group counts divisible by 8: the MFMA kernel copies scales eight groups
+    # at a time (the other MFMA shapes above take the per-group copy)
+    (200, 500, 1024), (130, 300, 2048),
     # the largest K whose scales the small-batch kernel keeps in LDS, and the
     # next group up, which a small batch runs on the MFMA kernel instead
     (3, 70, 49152), (8, 96, 49280),
@@ -193,6 +196,28 @@ def test_small_batch_unaligned_scales(ql):
     sc_view.copy_(dev_u16(sc))
     assert sc_view.data_ptr() % 16 == 2
     y = ql.forward(dev_u16(x), dev(qw), sc_view)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_u16(y), ref)
+
+
+@pytest.mark.parametrize("ws", [False, True])
+def test_mfma_unaligned_scales(ql, ws):
+    """16 groups (a multiple of 8) but scales only 2-byte aligned: the MFMA
+    kernel falls back from eight-group scale copies to per-group copies."""
+    M, N, K = 150, 300, 2048
+    say(f"mfma unaligned scales M={M} N={N} K={K} ws={ws}")
+    x = synth.ternary_bf16(15, M, K)
+    qw = synth.random_packed_bytes(16, N, K)
+    sc = synth.pow2_scales_f16(16, N, K // 128)
+    ref = O.f64_to_bf16_bits(O.qlinear_ref(x, qw, sc))
+    buf = torch.zeros(N * (K // 128) + 8, dtype=torch.int16, device="cuda")
+    sc_view = buf[1:1 + N * (K // 128)].view(N, K // 128)
+    sc_view.copy_(dev_u16(sc))
+    assert sc_view.data_ptr() % 16 == 2
+    xd = dev_u16(x)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    wsb = torch.empty(ql.workspace_bytes(M, K), dtype=torch.uint8, device="cuda") if ws else None
+    ql.forward_ex(xd, dev(qw), sc_view, y, ql.EPI_NONE, wsb)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host_u16(y), ref)
 
