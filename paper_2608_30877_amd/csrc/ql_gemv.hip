@@ -1,6 +1,7 @@
 // Small-batch (M <= 16) int4-weight projection: weight bytes bound the run.
 //
-// Each workgroup (4 waves) owns 64 output columns over the full K; wave w
+// Each workgroup (4 waves) owns 16 F output columns (F = 3, 4 or 6 column
+// fragments of 16, chosen per N by gemv_fragments) over the full K; wave w
 // takes the pairs of scale groups (2u, 2u+1), u = w, w+4, w+8, ..., and loads
 // a pair's codes back to back, so that each wave reads whole 128-byte lines
 // of its weight rows (with a line's halves spread over two waves the same
@@ -15,7 +16,7 @@
 // 16x16x32 MFMA chain against the (at most 16) activation rows; the rows'
 // group sums come from one more MFMA chain against a constant -136 operand,
 // which starts each chain so that it yields the exact code dot product.  The
-// workgroup's scales (64 columns x G, one contiguous block of the scale
+// workgroup's scales (16 F columns x G, one contiguous block of the scale
 // matrix) are copied into LDS once at the start: per-group scale loads would
 // cost as many memory instructions as the codes themselves.  The partial
 // sums of the four waves are then reduced through LDS (the wavefront
@@ -30,10 +31,17 @@ namespace ql {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kCols = 64;   // output columns per workgroup
-// LDS ahead of the scales: the waves' activation tiles, later the partial sums
-constexpr int kGemvTileBytes = kWaves * 256 * 16;
-static_assert((kWaves - 1) * 4 * 64 * 16 <= kGemvTileBytes, "partial sums fit the tiles");
+// F 16-column fragments per wave: the workgroup owns 16 F output columns.
+// LDS ahead of the scales: the waves' activation tiles, later the partial sums.
+template <int F>
+constexpr int tile_bytes() {
+  return kWaves * 256 * 16 > (kWaves - 1) * F * 64 * 16 ? kWaves * 256 * 16
+                                                        : (kWaves - 1) * F * 64 * 16;
+}
+template <int F>
+size_t lds_bytes(int64_t K) {
+  return (size_t)tile_bytes<F>() + (size_t)16 * F * (K / kGroup) * 2;
+}
 
 struct GemvParams {
   const uint16_t* x;
@@ -52,17 +60,19 @@ __device__ __forceinline__ int x_msk(int row) {
   return row ^ ((((row >> 2) ^ (row >> 3)) & 1) << 2);
 }
 
-// codes of a pair of consecutive groups (2 x 4 column fragments)
+// codes of a pair of consecutive groups (2 x F column fragments)
+template <int F>
 struct PairCodes {
-  u32x4 b[2][4];
+  u32x4 b[2][F];
 };
 // The pair's code loads back to back: the wave reads both 64-byte halves of
 // each 128-byte line of its 16 weight rows per fragment one right after the
 // other.  Group indices past the end are clamped (valid memory; never used).
-__device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[4], int g, int G,
-                                           PairCodes& d) {
+template <int F>
+__device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[F], int g, int G,
+                                           PairCodes<F>& d) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < F; ++j)
 #pragma unroll
     for (int e = 0; e < 2; ++e)
       d.b[e][j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)min(g + e, G - 1) * (kGroup / 2));
@@ -72,11 +82,11 @@ __device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[4], int 
 // loaded here, their latency covered by the other waves of the CU) go
 // through the wave's LDS tile into the operand layout (rows past M hold stale
 // values; they only reach output rows that are never stored).
-template <int XQ>
-__device__ __forceinline__ void compute_group(const u32x4 (&b)[4],
+template <int XQ, int F>
+__device__ __forceinline__ void compute_group(const u32x4 (&b)[F],
                                               const uint16_t* const (&xsrc)[XQ], u32x4* xt,
                                               const int (&xdst)[XQ], const uint16_t* sS, int G,
-                                              int g, int h, int lr, f32x4 (&acc)[4]) {
+                                              int g, int h, int lr, f32x4 (&acc)[F]) {
   const bf16x8 neg = neg136x8();
   u32x4 xa[XQ];
 #pragma unroll
@@ -90,17 +100,19 @@ __device__ __forceinline__ void compute_group(const u32x4 (&b)[4],
   f32x4 nc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < 4; ++s) nc = mfma16x16x32(a[s], neg, nc);
-  f32x4 c[4] = {nc, nc, nc, nc};
+  f32x4 c[F];
+#pragma unroll
+  for (int j = 0; j < F; ++j) c[j] = nc;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < F; ++j) {
       const uint32_t wv = s == 0 ? b[j].x : s == 1 ? b[j].y : s == 2 ? b[j].z : b[j].w;
       c[j] = mfma16x16x32(a[s], unpack_offset_codes(wv), c[j]);
     }
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] += c[j] * f16_to_f32(sS[(j * 16 + lr) * G + g]);
+  for (int j = 0; j < F; ++j) acc[j] += c[j] * f16_to_f32(sS[(j * 16 + lr) * G + g]);
 }
 
 // Copy `count` binary16 values from src to LDS dst with all of a thread's
@@ -143,15 +155,16 @@ __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, 
   }
 }
 
-// three workgroups (twelve waves) per CU
-template <int EPI, int XQ>
-__global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
-  // [kWaves][256] activation tiles (after the loop: [kWaves-1][4][64] partial
+// 12 / F workgroups (48 / F waves) per CU: 4 for F = 3, 3 for F = 4, 2 for F = 6
+template <int EPI, int XQ, int F>
+__global__ __launch_bounds__(kWaves * 64, 12 / F) void k_gemv(GemvParams p) {
+  constexpr int kCols = 16 * F;
+  // [kWaves][256] activation tiles (after the loop: [kWaves-1][F][64] partial
   // sums), then the scales [kCols][G]
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4* xtiles = reinterpret_cast<u32x4*>(smem);
   f32x4* red = reinterpret_cast<f32x4*>(smem);
-  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + kGemvTileBytes);
+  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + tile_bytes<F>());
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = lane >> 4, lr = lane & 15;
   const int64_t n0 = (int64_t)blockIdx.x * kCols;
@@ -160,9 +173,9 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
   // rows past M and columns past N read valid (clamped) memory; their
   // results are never stored (nor are the columns whose scales the
   // workgroup's copy leaves unset)
-  const uint8_t* wrow[4];
+  const uint8_t* wrow[F];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < F; ++j) {
     const int64_t col = std::min<int64_t>(n0 + j * 16 + lr, p.N - 1);
     wrow[j] = p.qw + col * (p.K / 2) + h * 16;
   }
@@ -176,9 +189,9 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
   }
   u32x4* xt = xtiles + wave * 256;
 
-  f32x4 acc[4];
+  f32x4 acc[F];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < F; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // this wave's groups: pairs of consecutive groups (2u, 2u+1) for u = wave,
   // wave + kWaves, ...; the code loads of the next two pairs are in flight
@@ -186,7 +199,7 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
   const int U = (G + 1) / 2;
   const int TU = U > wave ? (U - wave + kWaves - 1) / kWaves : 0;
   const auto first = [&](int t) { return 2 * (wave + kWaves * t); };
-  PairCodes cb[2];
+  PairCodes<F> cb[2];
   load_codes(wrow, first(0), G, cb[0]);
   load_codes(wrow, first(1), G, cb[1]);
   const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
@@ -199,8 +212,8 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
       const int t = t0 + d;
       if (t < TU) {
         const int g = first(t);
-        compute_group<XQ>(cb[d].b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
-        if (g + 1 < G) compute_group<XQ>(cb[d].b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
+        compute_group<XQ, F>(cb[d].b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
+        if (g + 1 < G) compute_group<XQ, F>(cb[d].b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
       }
       load_codes(wrow, first(t + 2), G, cb[d]);
     }
@@ -210,16 +223,16 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
   __syncthreads();
   if (wave > 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) red[((wave - 1) * 4 + j) * 64 + lane] = acc[j];
+    for (int j = 0; j < F; ++j) red[((wave - 1) * F + j) * 64 + lane] = acc[j];
   }
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
   for (int w = 0; w < kWaves - 1; ++w)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] += red[(w * 4 + j) * 64 + lane];
+    for (int j = 0; j < F; ++j) acc[j] += red[(w * F + j) * 64 + lane];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < F; ++j) {
     const int64_t col = n0 + j * 16 + lr;
     if (col >= p.N) continue;
 #pragma unroll
@@ -241,8 +254,33 @@ __global__ __launch_bounds__(kWaves * 64, 3) void k_gemv(GemvParams p) {
 
 }  // namespace
 
-size_t gemv_lds_bytes(int64_t K) {
-  return (size_t)kGemvTileBytes + (size_t)kCols * (K / kGroup) * 2;
+// The 16-column fragments per wave fall back to 4 (the smallest LDS need of
+// the shapes that balance: 64 columns per workgroup, three per CU).
+size_t gemv_lds_bytes(int64_t K) { return lds_bytes<4>(K); }
+
+// Fragments per wave for N columns.  Every workgroup re-reads the whole
+// activation block, so wide workgroups save load instructions, while the
+// workgroups must spread evenly over the 256 CUs: with F fragments (16 F
+// columns per workgroup, up to 12 / F workgroups resident per CU) the
+// busiest CU runs ceil(workgroups / 256) * F fragment-columns.  The
+// smallest such load wins, ties going to the wider workgroup; the scale
+// block must fit the LDS bound.  N = 49152: 6 (512 workgroups, 2 per CU);
+// N = 36864: 3 (768, 3 per CU); N = 12288: 3 (256, 1 per CU).
+int gemv_fragments(int64_t N, int64_t K) {
+  constexpr int64_t kCUs = 256;
+  int best = 4;
+  int64_t best_load = -1;
+  for (const int F : {6, 4, 3}) {
+    const size_t lds = F == 6 ? lds_bytes<6>(K) : F == 4 ? lds_bytes<4>(K) : lds_bytes<3>(K);
+    if (lds > kGemvMaxLds) continue;
+    const int64_t wgs = (N + 16 * F - 1) / (16 * F);
+    const int64_t load = (wgs + kCUs - 1) / kCUs * F;
+    if (best_load < 0 || load < best_load) {
+      best = F;
+      best_load = load;
+    }
+  }
+  return best;
 }
 
 hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
@@ -259,16 +297,23 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   p.N = (int)N;
   p.K = (int)K;
   p.G = (int)(K / kGroup);
-  const size_t lds = gemv_lds_bytes(K);
-  const dim3 grid((unsigned)((N + kCols - 1) / kCols)), block(kWaves * 64);
+  const int F = gemv_fragments(N, K);
   const int xq = (int)((M + 3) / 4);   // contiguous 4-row activation loads per group
-#define QL_GEMV(E, Q) hipLaunchKernelGGL((k_gemv<E, Q>), grid, block, lds, s, p)
+#define QL_GEMV(E, Q, FF)                                                             \
+  hipLaunchKernelGGL((k_gemv<E, Q, FF>), dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), \
+                     dim3(kWaves * 64), lds_bytes<FF>(K), s, p)
+#define QL_GEMV_F(E, Q)                  \
+  switch (F) {                           \
+    case 6: QL_GEMV(E, Q, 6); break;     \
+    case 3: QL_GEMV(E, Q, 3); break;     \
+    default: QL_GEMV(E, Q, 4); break;    \
+  }
 #define QL_GEMV_Q(E)                     \
   switch (xq) {                          \
-    case 1: QL_GEMV(E, 1); break;        \
-    case 2: QL_GEMV(E, 2); break;        \
-    case 3: QL_GEMV(E, 3); break;        \
-    default: QL_GEMV(E, 4); break;       \
+    case 1: QL_GEMV_F(E, 1); break;      \
+    case 2: QL_GEMV_F(E, 2); break;      \
+    case 3: QL_GEMV_F(E, 3); break;      \
+    default: QL_GEMV_F(E, 4); break;     \
   }
   switch (epilogue) {
     case 1: QL_GEMV_Q(1); break;
@@ -276,6 +321,7 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
     default: QL_GEMV_Q(0); break;
   }
 #undef QL_GEMV_Q
+#undef QL_GEMV_F
 #undef QL_GEMV
   return hipGetLastError();
 }

@@ -111,6 +111,9 @@ SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel (32-, 64- and 128-row t
     # the largest K whose scales the small-batch kernel keeps in LDS, and the
     # next group up, which a small batch runs on the MFMA kernel instead
     (3, 70, 49152), (8, 96, 49280),
+    # small batches whose column count selects workgroups of 6 and 4 column
+    # fragments (the shapes above take 3), each with a ragged last workgroup
+    (5, 24566, 384), (7, 12304, 640),
 ]
 
 
