@@ -114,6 +114,9 @@ SHAPES = [  # (M, N, K): small-batch kernel, MFMA kernel (32-, 64- and 128-row t
     # small batches whose column count selects workgroups of 6 and 4 column
     # fragments (the shapes above take 3), each with a ragged last workgroup
     (5, 24566, 384), (7, 12304, 640),
+    # N = 49152 (512 workgroups of 96 columns) with one group and with ten:
+    # some waves get no group and contribute zero partial sums
+    (3, 49152, 128), (8, 49152, 1280),
 ]
 
 
