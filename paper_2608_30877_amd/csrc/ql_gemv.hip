@@ -9,10 +9,14 @@
 // load per 16-column fragment (the lane's 32 codes); the group's
 // activations (M rows x 256 bytes) come in ceil(M/4) contiguous loads of 4
 // rows each and reach the MFMA operand layout through a wave-private LDS
-// tile, which costs far less than four 16-row loads in that layout.  All
-// code loads are unconditional (indices past the last group are clamped):
-// the codes of two pairs stay in flight in registers, and the compiler's
-// counted waits let them fly while a pair is computed.  The codes are unpacked to bf16 136 + q and run through a
+// tile, which costs far less than four 16-row loads in that layout.  With
+// pair tiles (F = 6, and F = 3 where the LDS allows) each wave keeps two
+// tiles and the next pair's activation loads fly while a pair is computed;
+// loaded just before use, their L2 round trip stalled the wave once per
+// group.  All loads are unconditional (indices past the last group are
+// clamped): the codes of two pairs stay in flight in registers, and the
+// compiler's counted waits let them fly while a pair is computed.  The codes
+// are unpacked to bf16 136 + q and run through a
 // 16x16x32 MFMA chain against the (at most 16) activation rows; the rows'
 // group sums come from one more MFMA chain against a constant -136 operand,
 // which starts each chain so that it yields the exact code dot product.  The
@@ -33,14 +37,18 @@ namespace {
 constexpr int kWaves = 4;
 // F 16-column fragments per wave: the workgroup owns 16 F output columns.
 // LDS ahead of the scales: the waves' activation tiles, later the partial sums.
-template <int F>
+// PT (pair tiles): each wave keeps two activation tiles (a pair of groups)
+// and loads the next pair's activations while one pair is computed;
+// otherwise one tile, loaded and used within a group.
+template <int F, bool PT>
 constexpr int tile_bytes() {
-  return kWaves * 256 * 16 > (kWaves - 1) * F * 64 * 16 ? kWaves * 256 * 16
-                                                        : (kWaves - 1) * F * 64 * 16;
+  return kWaves * 256 * 16 * (PT ? 2 : 1) > (kWaves - 1) * F * 64 * 16
+             ? kWaves * 256 * 16 * (PT ? 2 : 1)
+             : (kWaves - 1) * F * 64 * 16;
 }
-template <int F>
+template <int F, bool PT>
 size_t lds_bytes(int64_t K) {
-  return (size_t)tile_bytes<F>() + (size_t)16 * F * (K / kGroup) * 2;
+  return (size_t)tile_bytes<F, PT>() + (size_t)16 * F * (K / kGroup) * 2;
 }
 
 struct GemvParams {
@@ -82,17 +90,30 @@ __device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[F], int 
 // loaded here, their latency covered by the other waves of the CU) go
 // through the wave's LDS tile into the operand layout (rows past M hold stale
 // values; they only reach output rows that are never stored).
+template <int F>
+__device__ __forceinline__ void compute_tile(const u32x4 (&b)[F], const u32x4* xt,
+                                             const uint16_t* sS, int G, int g, int h, int lr,
+                                             f32x4 (&acc)[F]);
+
 template <int XQ, int F>
 __device__ __forceinline__ void compute_group(const u32x4 (&b)[F],
                                               const uint16_t* const (&xsrc)[XQ], u32x4* xt,
                                               const int (&xdst)[XQ], const uint16_t* sS, int G,
                                               int g, int h, int lr, f32x4 (&acc)[F]) {
-  const bf16x8 neg = neg136x8();
   u32x4 xa[XQ];
 #pragma unroll
   for (int q = 0; q < XQ; ++q) xa[q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)g * kGroup);
 #pragma unroll
   for (int q = 0; q < XQ; ++q) xt[xdst[q]] = xa[q];
+  compute_tile<F>(b, xt, sS, G, g, h, lr, acc);
+}
+
+// A group whose activations are already in the wave's LDS tile xt.
+template <int F>
+__device__ __forceinline__ void compute_tile(const u32x4 (&b)[F], const u32x4* xt,
+                                             const uint16_t* sS, int G, int g, int h, int lr,
+                                             f32x4 (&acc)[F]) {
+  const bf16x8 neg = neg136x8();
   bf16x8 a[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
@@ -156,15 +177,23 @@ __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, 
 }
 
 // 12 / F workgroups (48 / F waves) per CU: 4 for F = 3, 3 for F = 4, 2 for F = 6
-template <int EPI, int XQ, int F>
-__global__ __launch_bounds__(kWaves * 64, 12 / F) void k_gemv(GemvParams p) {
+// workgroups per CU the launch bounds provide for: 12 / F (4 waves each),
+// but 3 for F = 3 (no shape that picks F = 3 has more per CU; the registers
+// then hold the pair tiles' prefetched activations)
+template <int F>
+constexpr int gemv_wgs_per_cu() {
+  return F == 3 ? 3 : 12 / F;
+}
+
+template <int EPI, int XQ, int F, bool PT>
+__global__ __launch_bounds__(kWaves * 64, gemv_wgs_per_cu<F>()) void k_gemv(GemvParams p) {
   constexpr int kCols = 16 * F;
   // [kWaves][256] activation tiles (after the loop: [kWaves-1][F][64] partial
   // sums), then the scales [kCols][G]
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4* xtiles = reinterpret_cast<u32x4*>(smem);
   f32x4* red = reinterpret_cast<f32x4*>(smem);
-  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + tile_bytes<F>());
+  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + tile_bytes<F, PT>());
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = lane >> 4, lr = lane & 15;
   const int64_t n0 = (int64_t)blockIdx.x * kCols;
@@ -187,7 +216,7 @@ __global__ __launch_bounds__(kWaves * 64, 12 / F) void k_gemv(GemvParams p) {
     xsrc[q] = p.x + (int64_t)min(row, p.M - 1) * p.ldx + ch * 8;
     xdst[q] = row * 16 + (ch ^ x_msk(row));
   }
-  u32x4* xt = xtiles + wave * 256;
+  u32x4* xt = xtiles + wave * 256 * (PT ? 2 : 1);
 
   f32x4 acc[F];
 #pragma unroll
@@ -206,16 +235,47 @@ __global__ __launch_bounds__(kWaves * 64, 12 / F) void k_gemv(GemvParams p) {
   copy_scales(p.sc + n0 * G, sS, cols * G);
   __syncthreads();
 
-  for (int t0 = 0; t0 < TU; t0 += 2) {
+  if constexpr (PT) {
+    // activations of the pair being computed come from loads issued while
+    // the pair before it was computed (group indices clamped: valid memory)
+    u32x4 xa[2][XQ];
+    const auto load_acts = [&](int g) {
 #pragma unroll
-    for (int d = 0; d < 2; ++d) {
-      const int t = t0 + d;
-      if (t < TU) {
-        const int g = first(t);
-        compute_group<XQ, F>(cb[d].b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
-        if (g + 1 < G) compute_group<XQ, F>(cb[d].b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int q = 0; q < XQ; ++q)
+          xa[e][q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)min(g + e, G - 1) * kGroup);
+    };
+    load_acts(first(0));
+    for (int t0 = 0; t0 < TU; t0 += 2) {
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        const int t = t0 + d;
+        if (t < TU) {
+          const int g = first(t);
+#pragma unroll
+          for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = xa[e][q];
+          load_acts(first(t + 1));
+          compute_tile<F>(cb[d].b[0], xt, sS, G, g, h, lr, acc);
+          if (g + 1 < G) compute_tile<F>(cb[d].b[1], xt + 256, sS, G, g + 1, h, lr, acc);
+        }
+        load_codes(wrow, first(t + 2), G, cb[d]);
       }
-      load_codes(wrow, first(t + 2), G, cb[d]);
+    }
+  } else {
+    for (int t0 = 0; t0 < TU; t0 += 2) {
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        const int t = t0 + d;
+        if (t < TU) {
+          const int g = first(t);
+          compute_group<XQ, F>(cb[d].b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
+          if (g + 1 < G) compute_group<XQ, F>(cb[d].b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
+        }
+        load_codes(wrow, first(t + 2), G, cb[d]);
+      }
     }
   }
 
@@ -254,9 +314,10 @@ __global__ __launch_bounds__(kWaves * 64, 12 / F) void k_gemv(GemvParams p) {
 
 }  // namespace
 
-// The 16-column fragments per wave fall back to 4 (the smallest LDS need of
-// the shapes that balance: 64 columns per workgroup, three per CU).
-size_t gemv_lds_bytes(int64_t K) { return lds_bytes<4>(K); }
+// The 16-column fragments per wave fall back to 4 with single tiles (the
+// smallest LDS need of the shapes that balance: 64 columns per workgroup,
+// three per CU).
+size_t gemv_lds_bytes(int64_t K) { return lds_bytes<4, false>(K); }
 
 // Fragments per wave for N columns.  Every workgroup re-reads the whole
 // activation block, so wide workgroups save load instructions, while the
@@ -271,7 +332,8 @@ int gemv_fragments(int64_t N, int64_t K) {
   int best = 4;
   int64_t best_load = -1;
   for (const int F : {6, 4, 3}) {
-    const size_t lds = F == 6 ? lds_bytes<6>(K) : F == 4 ? lds_bytes<4>(K) : lds_bytes<3>(K);
+    const size_t lds = F == 6 ? lds_bytes<6, true>(K)
+                       : F == 4 ? lds_bytes<4, false>(K) : lds_bytes<3, false>(K);
     if (lds > kGemvMaxLds) continue;
     const int64_t wgs = (N + 16 * F - 1) / (16 * F);
     const int64_t load = (wgs + kCUs - 1) / kCUs * F;
@@ -298,16 +360,19 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   p.K = (int)K;
   p.G = (int)(K / kGroup);
   const int F = gemv_fragments(N, K);
+  // pair tiles for F = 6 (within the LDS bound by the choice above) and
+  // F = 3 when two workgroups still fit a CU's LDS; F = 4 keeps single tiles
+  // (its three workgroups per CU leave no registers for the prefetch)
+  const bool pt = F == 6 || (F == 3 && lds_bytes<3, true>(K) <= 80 * 1024);
   const int xq = (int)((M + 3) / 4);   // contiguous 4-row activation loads per group
-#define QL_GEMV(E, Q, FF)                                                             \
-  hipLaunchKernelGGL((k_gemv<E, Q, FF>), dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), \
-                     dim3(kWaves * 64), lds_bytes<FF>(K), s, p)
-#define QL_GEMV_F(E, Q)                  \
-  switch (F) {                           \
-    case 6: QL_GEMV(E, Q, 6); break;     \
-    case 3: QL_GEMV(E, Q, 3); break;     \
-    default: QL_GEMV(E, Q, 4); break;    \
-  }
+#define QL_GEMV(E, Q, FF, PP)                                                                 \
+  hipLaunchKernelGGL((k_gemv<E, Q, FF, PP>), dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), \
+                     dim3(kWaves * 64), (lds_bytes<FF, PP>(K)), s, p)
+#define QL_GEMV_F(E, Q)                             \
+  if (F == 6) QL_GEMV(E, Q, 6, true);               \
+  else if (F == 3 && pt) QL_GEMV(E, Q, 3, true);    \
+  else if (F == 3) QL_GEMV(E, Q, 3, false);         \
+  else QL_GEMV(E, Q, 4, false);
 #define QL_GEMV_Q(E)                     \
   switch (xq) {                          \
     case 1: QL_GEMV_F(E, 1); break;      \
