@@ -236,6 +236,8 @@ def bench_stack(args, ql, synth, torch):
                 out["ragged"]["pairs_per_s"] / out["with_attention"]["pairs_per_s"], 4)
     if not args.no_sweep:
         out["batch_sweep"] = bench_batch_sweep(ql, synth, torch, arr, L, d, dff)
+        out["small_batch_stack"] = bench_stack_small_batch(ql, synth, torch, arr, L, d, dff,
+                                                           resident)
     if not args.no_streamed:
         out["host_streamed"] = bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d,
                                                     dff, pairs, ms)
@@ -311,6 +313,32 @@ def bench_batch_sweep(ql, synth, torch, arr, L, d, dff, pair_counts=(1, 2, 4, 16
                     "tflops": round(flops / (ms / 1e3) / 1e12, 1)})
         del ws, h0, h
     return res
+
+
+def bench_stack_small_batch(ql, synth, torch, arr, L, d, dff, resident, M=8, steps=3):
+    """The same resident stack on a batch of M = 8 tokens: every projection
+    runs the small-batch kernel, so a forward streams all resident weight
+    bytes once; two warmup and `steps` timed forwards."""
+    ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
+    h0 = torch.from_numpy(synth.residual_f32(synth.SEED_STACK + 1000, M, d)).cuda()
+    h = torch.empty_like(h0)
+    for _ in range(2):       # warm-up: the clocks settle under the memory-bound loop
+        h.copy_(h0)
+        ql.stack_forward(arr, h, dff, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        h.copy_(h0)
+        ql.stack_forward(arr, h, dff, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    gbs = resident / (ms * 1e-3) / 1e9
+    del ws, h0, h
+    return {"tokens": M, "layers": L, "ms_per_step": round(ms, 2),
+            "tokens_per_s": round(M / (ms * 1e-3), 1),
+            "weight_GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 STREAM_POOL = 16   # distinct blocks kept in page-locked host memory for the streamed variant
@@ -471,10 +499,10 @@ def bench_small_batch(ql, synth, torch, reps=50, copies=4):
     del w
     x = torch.from_numpy(synth.activations_bf16(synth.SEED_GEMV, M, K).view("int16")).cuda()
     y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    # warm-up long enough for the clock to settle after the packing (a short
-    # one left the first timed loop ~7 % slow), then the median of three
-    # timed loops
-    for i in range(reps):
+    # warm-up long enough for the clocks to reach their steady state under
+    # this memory-bound loop (about 20 ms of it; after 50 launches the timed
+    # loops still ran ~8 % slow), then the median of three timed loops
+    for i in range(400):
         ql.forward(x, *mats[i % copies], out=y)
     times = []
     for _ in range(3):
