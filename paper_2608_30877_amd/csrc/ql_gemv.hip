@@ -1,8 +1,9 @@
 // Small-batch (M <= 16) int4-weight projection: weight bytes bound the run.
 //
-// Each workgroup (4 waves) owns 16 F output columns (F = 3, 4 or 6 column
-// fragments of 16, chosen per N by gemv_fragments) over the full K; wave w
-// takes the pairs of scale groups (2u, 2u+1), u = w, w+4, w+8, ..., and loads
+// Each workgroup (W = 4 waves, or 8 when it is the only one on its CU) owns
+// 16 F output columns (F = 3, 4 or 6 column fragments of 16, chosen per N by
+// gemv_fragments) over the full K; wave w takes the pairs of scale groups
+// (2u, 2u+1), u = w, w+W, w+2W, ..., and loads
 // a pair's codes back to back, so that each wave reads whole 128-byte lines
 // of its weight rows (with a line's halves spread over two waves the same
 // reads stream about 10 % slower).  Per group, each lane issues one 16-byte
@@ -40,15 +41,15 @@ constexpr int kWaves = 4;
 // PT (pair tiles): each wave keeps two activation tiles (a pair of groups)
 // and loads the next pair's activations while one pair is computed;
 // otherwise one tile, loaded and used within a group.
-template <int F, bool PT>
+// W waves per workgroup (4, or 8 for one workgroup per CU).
+template <int F, bool PT, int W = kWaves>
 constexpr int tile_bytes() {
-  return kWaves * 256 * 16 * (PT ? 2 : 1) > (kWaves - 1) * F * 64 * 16
-             ? kWaves * 256 * 16 * (PT ? 2 : 1)
-             : (kWaves - 1) * F * 64 * 16;
+  return W * 256 * 16 * (PT ? 2 : 1) > (W - 1) * F * 64 * 16 ? W * 256 * 16 * (PT ? 2 : 1)
+                                                             : (W - 1) * F * 64 * 16;
 }
-template <int F, bool PT>
+template <int F, bool PT, int W = kWaves>
 size_t lds_bytes(int64_t K) {
-  return (size_t)tile_bytes<F, PT>() + (size_t)16 * F * (K / kGroup) * 2;
+  return (size_t)tile_bytes<F, PT, W>() + (size_t)16 * F * (K / kGroup) * 2;
 }
 
 struct GemvParams {
@@ -139,8 +140,9 @@ __device__ __forceinline__ void compute_tile(const u32x4 (&b)[F], const u32x4* x
 // Copy `count` binary16 values from src to LDS dst with all of a thread's
 // loads of a batch in flight together (16-byte loads when src is 16-byte
 // aligned, which also makes dst's 16-byte slots line up).
+template <int W>
 __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, int count) {
-  const int t = threadIdx.x, nt = kWaves * 64;
+  const int t = threadIdx.x, nt = W * 64;
   int done = 0;
   if (((uintptr_t)src & 15u) == 0) {
     const int nv = count / 8;
@@ -180,20 +182,21 @@ __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, 
 // workgroups per CU the launch bounds provide for: 12 / F (4 waves each),
 // but 3 for F = 3 (no shape that picks F = 3 has more per CU; the registers
 // then hold the pair tiles' prefetched activations)
-template <int F>
+template <int F, int W>
 constexpr int gemv_wgs_per_cu() {
-  return F == 3 ? 3 : 12 / F;
+  return W != kWaves ? 1 : F == 3 ? 3 : 12 / F;
 }
 
-template <int EPI, int XQ, int F, bool PT>
-__global__ __launch_bounds__(kWaves * 64, gemv_wgs_per_cu<F>()) void k_gemv(GemvParams p) {
+template <int EPI, int XQ, int F, bool PT, int W>
+__global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(GemvParams p) {
+  constexpr int kWaves = W;
   constexpr int kCols = 16 * F;
   // [kWaves][256] activation tiles (after the loop: [kWaves-1][F][64] partial
   // sums), then the scales [kCols][G]
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4* xtiles = reinterpret_cast<u32x4*>(smem);
   f32x4* red = reinterpret_cast<f32x4*>(smem);
-  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + tile_bytes<F, PT>());
+  uint16_t* sS = reinterpret_cast<uint16_t*>(smem + tile_bytes<F, PT, W>());
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = lane >> 4, lr = lane & 15;
   const int64_t n0 = (int64_t)blockIdx.x * kCols;
@@ -232,7 +235,7 @@ __global__ __launch_bounds__(kWaves * 64, gemv_wgs_per_cu<F>()) void k_gemv(Gemv
   load_codes(wrow, first(0), G, cb[0]);
   load_codes(wrow, first(1), G, cb[1]);
   const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
-  copy_scales(p.sc + n0 * G, sS, cols * G);
+  copy_scales<W>(p.sc + n0 * G, sS, cols * G);
   __syncthreads();
 
   if constexpr (PT) {
@@ -364,15 +367,20 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   // F = 3 when two workgroups still fit a CU's LDS; F = 4 keeps single tiles
   // (its three workgroups per CU leave no registers for the prefetch)
   const bool pt = F == 6 || (F == 3 && lds_bytes<3, true>(K) <= 80 * 1024);
+  // one workgroup per CU (F = 3, at most 256 workgroups): eight waves split
+  // its groups, so twice the code bytes are in flight per CU
+  const bool w8 = F == 3 && pt && (N + 47) / 48 <= 256 && lds_bytes<3, true, 8>(K) <= 160 * 1024;
   const int xq = (int)((M + 3) / 4);   // contiguous 4-row activation loads per group
-#define QL_GEMV(E, Q, FF, PP)                                                                 \
-  hipLaunchKernelGGL((k_gemv<E, Q, FF, PP>), dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), \
-                     dim3(kWaves * 64), (lds_bytes<FF, PP>(K)), s, p)
-#define QL_GEMV_F(E, Q)                             \
-  if (F == 6) QL_GEMV(E, Q, 6, true);               \
-  else if (F == 3 && pt) QL_GEMV(E, Q, 3, true);    \
-  else if (F == 3) QL_GEMV(E, Q, 3, false);         \
-  else QL_GEMV(E, Q, 4, false);
+#define QL_GEMV(E, Q, FF, PP, WW)                                                             \
+  hipLaunchKernelGGL((k_gemv<E, Q, FF, PP, WW>),                                              \
+                     dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), dim3(WW * 64),          \
+                     (lds_bytes<FF, PP, WW>(K)), s, p)
+#define QL_GEMV_F(E, Q)                                 \
+  if (F == 6) QL_GEMV(E, Q, 6, true, 4);                \
+  else if (F == 3 && w8) QL_GEMV(E, Q, 3, true, 8);     \
+  else if (F == 3 && pt) QL_GEMV(E, Q, 3, true, 4);     \
+  else if (F == 3) QL_GEMV(E, Q, 3, false, 4);          \
+  else QL_GEMV(E, Q, 4, false, 4);
 #define QL_GEMV_Q(E)                     \
   switch (xq) {                          \
     case 1: QL_GEMV_F(E, 1); break;      \
