@@ -318,7 +318,8 @@ def bench_batch_sweep(ql, synth, torch, arr, L, d, dff, pair_counts=(1, 2, 4, 16
 def bench_stack_small_batch(ql, synth, torch, arr, L, d, dff, resident, M=8, steps=3):
     """The same resident stack on a batch of M = 8 tokens: every projection
     runs the small-batch kernel, so a forward streams all resident weight
-    bytes once; two warmup and `steps` timed forwards."""
+    bytes once; two warmup and `steps` timed forwards, launched eagerly and
+    replayed from one captured HIP graph."""
     ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
     h0 = torch.from_numpy(synth.residual_f32(synth.SEED_STACK + 1000, M, d)).cuda()
     h = torch.empty_like(h0)
@@ -335,10 +336,35 @@ def bench_stack_small_batch(ql, synth, torch, arr, L, d, dff, resident, M=8, ste
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     gbs = resident / (ms * 1e-3) / 1e9
-    del ws, h0, h
+    # the same forward captured in one HIP graph (576 kernel launches per
+    # forward: at ~200 us per block the host-side launch gaps show)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ql.stack_forward(arr, h, dff, ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        ql.stack_forward(arr, h, dff, ws)
+    for _ in range(2):
+        h.copy_(h0)
+        g.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        h.copy_(h0)
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_g = e0.elapsed_time(e1) / steps
+    gbs_g = resident / (ms_g * 1e-3) / 1e9
+    del g, ws, h0, h
     return {"tokens": M, "layers": L, "ms_per_step": round(ms, 2),
             "tokens_per_s": round(M / (ms * 1e-3), 1),
-            "weight_GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+            "weight_GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "graph_ms_per_step": round(ms_g, 2), "graph_weight_GBps": round(gbs_g, 1),
+            "graph_frac_hbm_peak": round(gbs_g / PEAK_HBM_GBS, 4)}
 
 
 STREAM_POOL = 16   # distinct blocks kept in page-locked host memory for the streamed variant
