@@ -2,30 +2,31 @@
 //
 // Each workgroup (W = 4 waves, or 8 when it is the only one on its CU) owns
 // 16 F output columns (F = 3, 4 or 6 column fragments of 16, chosen per N by
-// gemv_fragments) over the full K; wave w takes the pairs of scale groups
-// (2u, 2u+1), u = w, w+W, w+2W, ..., and loads
-// a pair's codes back to back, so that each wave reads whole 128-byte lines
-// of its weight rows (with a line's halves spread over two waves the same
-// reads stream about 10 % slower).  Per group, each lane issues one 16-byte
-// load per 16-column fragment (the lane's 32 codes); the group's
-// activations (M rows x 256 bytes) come in ceil(M/4) contiguous loads of 4
-// rows each and reach the MFMA operand layout through a wave-private LDS
-// tile, which costs far less than four 16-row loads in that layout.  With
-// pair tiles (F = 6, and F = 3 where the LDS allows) each wave keeps two
-// tiles and the next pair's activation loads fly while a pair is computed;
-// loaded just before use, their L2 round trip stalled the wave once per
-// group.  All loads are unconditional (indices past the last group are
-// clamped): the codes of two pairs stay in flight in registers, and the
-// compiler's counted waits let them fly while a pair is computed.  The codes
-// are unpacked to bf16 136 + q and run through a
-// 16x16x32 MFMA chain against the (at most 16) activation rows; the rows'
-// group sums come from one more MFMA chain against a constant -136 operand,
-// which starts each chain so that it yields the exact code dot product.  The
-// workgroup's scales (16 F columns x G, one contiguous block of the scale
-// matrix) are copied into LDS once at the start: per-group scale loads would
-// cost as many memory instructions as the codes themselves.  The partial
-// sums of the four waves are then reduced through LDS (the wavefront
-// reduction) and the epilogue is applied.
+// gemv_fragments) over the full K.  Wave w takes the pairs of scale groups
+// (2u, 2u+1), u = w, w+W, w+2W, ..., and loads a pair's codes back to back,
+// so that each wave reads whole 128-byte lines of its weight rows (with a
+// line's halves spread over two waves the same reads stream about 10 %
+// slower).  Per group, each lane issues one 16-byte load per 16-column
+// fragment (the lane's 32 codes); the group's activations (M rows x 256
+// bytes) come in ceil(M/4) contiguous loads of 4 rows each and reach the MFMA
+// operand layout through a wave-private LDS tile, which costs far less than
+// four 16-row loads in that layout.  With pair tiles (F = 6, and F = 3 where
+// the LDS allows) each wave keeps two tiles and the next pair's activation
+// loads fly while a pair is computed; loaded just before use, their L2 round
+// trip stalled the wave once per group.  All loads are unconditional
+// (indices past the last group are clamped): the codes of two pairs stay in
+// flight in registers, and the compiler's counted waits let them fly while a
+// pair is computed.
+//
+// The codes are unpacked to bf16 136 + q and run through a 16x16x32 MFMA
+// chain against the (at most 16) activation rows; the rows' group sums come
+// from one more MFMA chain against a constant -136 operand, which starts
+// each chain so that it yields the exact code dot product.  The workgroup's
+// scales (16 F columns x G, one contiguous block of the scale matrix) are
+// copied into LDS once at the start: per-group scale loads would cost as
+// many memory instructions as the codes themselves.  The partial sums of the
+// W waves are then reduced through LDS (the wavefront reduction) and the
+// epilogue is applied.
 #include <algorithm>
 
 #include "ql_device.h"
@@ -35,13 +36,10 @@ namespace ql {
 
 namespace {
 
-constexpr int kWaves = 4;
-// F 16-column fragments per wave: the workgroup owns 16 F output columns.
-// LDS ahead of the scales: the waves' activation tiles, later the partial sums.
-// PT (pair tiles): each wave keeps two activation tiles (a pair of groups)
-// and loads the next pair's activations while one pair is computed;
-// otherwise one tile, loaded and used within a group.
-// W waves per workgroup (4, or 8 for one workgroup per CU).
+constexpr int kWaves = 4;   // waves per workgroup unless it is alone on its CU
+// LDS ahead of the scales: the waves' activation tiles, later the partial
+// sums.  F: 16-column fragments per wave; PT (pair tiles): each wave keeps
+// two activation tiles (a pair of groups), otherwise one; W: waves.
 template <int F, bool PT, int W = kWaves>
 constexpr int tile_bytes() {
   return W * 256 * 16 * (PT ? 2 : 1) > (W - 1) * F * 64 * 16 ? W * 256 * 16 * (PT ? 2 : 1)
@@ -178,10 +176,9 @@ __device__ __forceinline__ void copy_scales(const uint16_t* src, uint16_t* dst, 
   }
 }
 
-// 12 / F workgroups (48 / F waves) per CU: 4 for F = 3, 3 for F = 4, 2 for F = 6
-// workgroups per CU the launch bounds provide for: 12 / F (4 waves each),
-// but 3 for F = 3 (no shape that picks F = 3 has more per CU; the registers
-// then hold the pair tiles' prefetched activations)
+// Workgroups per CU the launch bounds provide for: 12 / F of 4 waves (2 for
+// F = 6), but 3 for F = 3 (no shape that picks F = 3 has more per CU; the
+// registers then hold the pair tiles' prefetched activations), and 1 of 8.
 template <int F, int W>
 constexpr int gemv_wgs_per_cu() {
   return W != kWaves ? 1 : F == 3 ? 3 : 12 / F;
@@ -189,9 +186,8 @@ constexpr int gemv_wgs_per_cu() {
 
 template <int EPI, int XQ, int F, bool PT, int W>
 __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(GemvParams p) {
-  constexpr int kWaves = W;
   constexpr int kCols = 16 * F;
-  // [kWaves][256] activation tiles (after the loop: [kWaves-1][F][64] partial
+  // [W][256 or 512] activation tiles (after the loop: [W-1][F][64] partial
   // sums), then the scales [kCols][G]
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4* xtiles = reinterpret_cast<u32x4*>(smem);
@@ -226,11 +222,11 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   for (int j = 0; j < F; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // this wave's groups: pairs of consecutive groups (2u, 2u+1) for u = wave,
-  // wave + kWaves, ...; the code loads of the next two pairs are in flight
-  // while a pair is computed
+  // wave + W, ...; the code loads of the next two pairs are in flight while a
+  // pair is computed
   const int U = (G + 1) / 2;
-  const int TU = U > wave ? (U - wave + kWaves - 1) / kWaves : 0;
-  const auto first = [&](int t) { return 2 * (wave + kWaves * t); };
+  const int TU = U > wave ? (U - wave + W - 1) / W : 0;
+  const auto first = [&](int t) { return 2 * (wave + W * t); };
   PairCodes<F> cb[2];
   load_codes(wrow, first(0), G, cb[0]);
   load_codes(wrow, first(1), G, cb[1]);
@@ -291,7 +287,7 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
-  for (int w = 0; w < kWaves - 1; ++w)
+  for (int w = 0; w < W - 1; ++w)
 #pragma unroll
     for (int j = 0; j < F; ++j) acc[j] += red[(w * F + j) * 64 + lane];
 #pragma unroll
