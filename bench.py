@@ -542,11 +542,11 @@ def bench_small_batch(ql, synth, torch, reps=50, copies=4):
         times.append(e0.elapsed_time(e1) / reps * 1e-3)
     t = sorted(times)[1]
     wb = N * K // 2 + N * (K // 128) * 2
-    return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0, 2, 6>", "avg_us": round(t * 1e6, 2),
+    return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0, 2, 6, true, 4>", "avg_us": round(t * 1e6, 2),
             "weight_GBps": round(wb / t / 1e9, 1),
             "frac_hbm_peak": round(wb / t / 1e9 / PEAK_HBM_GBS, 4),
             "algorithmic_bytes": int(wb + 2 * M * K + 2 * M * N),
-            "traffic": measured_traffic("k_gemv<0, 2, 6>"), "traffic_unit": "bytes/launch"}
+            "traffic": measured_traffic("k_gemv<0, 2, 6, true, 4>"), "traffic_unit": "bytes/launch"}
 
 
 def bench_prefill(ql, synth, torch, reps=10):
