@@ -61,7 +61,9 @@ struct GemvParams {
 
 // Activation tile of one group in LDS: 16 rows x 16 chunks of 16 bytes, row r
 // storing chunk c at slot c ^ x_msk(r) so that the 16-row MFMA operand reads
-// are free of bank conflicts.
+// are free of bank conflicts.  Chunks are stored already in the codes' k
+// order (permute_chunk when written: ceil(M/4) permutes per group and lane
+// instead of four when read).
 __device__ __forceinline__ int x_msk(int row) {
   row &= 15;
   return row ^ ((((row >> 2) ^ (row >> 3)) & 1) << 2);
@@ -103,7 +105,7 @@ __device__ __forceinline__ void compute_group(const u32x4 (&b)[F],
 #pragma unroll
   for (int q = 0; q < XQ; ++q) xa[q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)g * kGroup);
 #pragma unroll
-  for (int q = 0; q < XQ; ++q) xt[xdst[q]] = xa[q];
+  for (int q = 0; q < XQ; ++q) xt[xdst[q]] = permute_chunk(xa[q]);
   compute_tile<F>(b, xt, sS, G, g, h, lr, acc);
 }
 
@@ -116,7 +118,7 @@ __device__ __forceinline__ void compute_tile(const u32x4 (&b)[F], const u32x4* x
   bf16x8 a[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
-    a[s] = as_bf16x8(permute_chunk(xt[lr * 16 + ((h * 4 + s) ^ x_msk(lr))]));
+    a[s] = as_bf16x8(xt[lr * 16 + ((h * 4 + s) ^ x_msk(lr))]);
   f32x4 nc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < 4; ++s) nc = mfma16x16x32(a[s], neg, nc);
@@ -230,22 +232,22 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   PairCodes<F> cb[2];
   load_codes(wrow, first(0), G, cb[0]);
   load_codes(wrow, first(1), G, cb[1]);
+  // pair tiles: the first pair's activations are requested before the scale
+  // copy, so that their round trip overlaps it
+  u32x4 xa[2][XQ];
+  const auto load_acts = [&](int g) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int q = 0; q < XQ; ++q)
+        xa[e][q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)min(g + e, G - 1) * kGroup);
+  };
+  if constexpr (PT) load_acts(first(0));
   const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
   copy_scales<W>(p.sc + n0 * G, sS, cols * G);
   __syncthreads();
 
   if constexpr (PT) {
-    // activations of the pair being computed come from loads issued while
-    // the pair before it was computed (group indices clamped: valid memory)
-    u32x4 xa[2][XQ];
-    const auto load_acts = [&](int g) {
-#pragma unroll
-      for (int e = 0; e < 2; ++e)
-#pragma unroll
-        for (int q = 0; q < XQ; ++q)
-          xa[e][q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)min(g + e, G - 1) * kGroup);
-    };
-    load_acts(first(0));
     for (int t0 = 0; t0 < TU; t0 += 2) {
 #pragma unroll
       for (int d = 0; d < 2; ++d) {
@@ -255,7 +257,7 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
 #pragma unroll
           for (int e = 0; e < 2; ++e)
 #pragma unroll
-            for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = xa[e][q];
+            for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = permute_chunk(xa[e][q]);
           load_acts(first(t + 1));
           compute_tile<F>(cb[d].b[0], xt, sS, G, g, h, lr, acc);
           if (g + 1 < G) compute_tile<F>(cb[d].b[1], xt + 256, sS, G, g + 1, h, lr, acc);
