@@ -13,7 +13,10 @@
 //   * a step runs four 32-k phases; in each, a wave reads its activation
 //     fragments from LDS, unpacks one 32-bit word of codes per column
 //     fragment into bf16 values 136 + q (exact; see unpack_offset_codes) and
-//     issues one 16x16x32 MFMA for each of its 4 x 4 output fragments;
+//     issues one 16x16x32 MFMA for each of its 4 x 4 output fragments (in
+//     the prepared form two consecutive words share their three shifts,
+//     done as 64-bit shifts: between MFMAs a 64-bit shift issues at the cost
+//     of a 32-bit one);
 //   * each fragment's chain of four MFMAs starts from the correction
 //     -136 * sum_k x[m][k], so its result is the integer-code dot product
 //     sum x*q (fp32), and one fp32 FMA applies the group's scale:
@@ -206,9 +209,9 @@ template <int IF>
 struct CopyJob {
   const GemmParams& p;
   const Offsets<IF>& o;
-  uint32_t os;
   int64_t m0;
   int g;
+  int64_t n0;
   Stage st;
   uint16_t* sb;  // the two eight-group scale buffers ([2][BN][8])
   int wave, lane;
@@ -220,6 +223,21 @@ struct CopyJob {
 // A_PER_WAVE: the wave's activation copies; the last two: its code copies.
 template <int IF>
 constexpr int kCopies = TileM<IF>::A_PER_WAVE + B_PER_WAVE + 1;
+
+__device__ __forceinline__ uint32_t scale_copy_offset(const GemmParams& p, int64_t n0, int wave,
+                                                      int lane) {
+  // 32-bit: a launch chunk keeps every byte offset below 2^31
+  return (uint32_t)min((int)n0 + ((wave - 2) & 3) * 64 + lane, p.N - 1) * (uint32_t)p.G;
+}
+// The lane id from a volatile statement: the scale copy offset derived from it
+// where the copy is issued cannot be hoisted out of the loop or kept live
+// across steps (a register held through the loop for it had been spilled,
+// and its reload waited for every copy in flight).
+__device__ __forceinline__ int lane_id_here() {
+  uint32_t l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return (int)l;
+}
 
 template <int IF, bool RAW, int J>
 __device__ __forceinline__ void issue_copy(const CopyJob<IF>& c) {
@@ -236,11 +254,12 @@ __device__ __forceinline__ void issue_copy(const CopyJob<IF>& c) {
         // buffer of batch g / 8 (read from step g on; the buffer's previous
         // batch was last read eight steps earlier)
         if ((c.g & 7) == 0)
-          copy16_to_lds(c.p.sc + c.g, c.os * 2,
+          copy16_to_lds(c.p.sc + c.g, scale_copy_offset(c.p, c.n0, wave, lane_id_here()) * 2,
                         (uint32_t)reinterpret_cast<uintptr_t>(
                             c.sb + ((c.g >> 3) & 1) * (BN * 8) + (wave - 2) * 64 * 8));
       } else {
-        copy_to_lds<2>(c.p.sc + c.g, c.os * 2, c.st.S + (wave - 2) * 64);
+        copy_to_lds<2>(c.p.sc + c.g, scale_copy_offset(c.p, c.n0, wave, lane_id_here()) * 2,
+                       c.st.S + (wave - 2) * 64);
       }
     }
   } else if constexpr (J <= NA) {
@@ -404,6 +423,18 @@ __device__ __forceinline__ bf16x8 unpack_word(uint32_t w) {
     return unpack_offset_codes(w);
 }
 
+// 8 codes from a word and its copies shifted right by 4, 8 and 12 bits
+// (the mask / XOR of unpack_offset_codes)
+__device__ __forceinline__ bf16x8 codes_from_shifts(uint32_t w0, uint32_t w4, uint32_t w8,
+                                                    uint32_t w12) {
+  u32x4 d;
+  d.x = (w0 & 0x000f000fu) ^ 0x43084308u;
+  d.y = (w4 & 0x000f000fu) ^ 0x43084308u;
+  d.z = (w8 & 0x000f000fu) ^ 0x43084308u;
+  d.w = (w12 & 0x000f000fu) ^ 0x43084308u;
+  return __builtin_bit_cast(bf16x8, d);
+}
+
 template <int S>
 __device__ __forceinline__ uint32_t word(const u32x4& v) {
   if constexpr (S == 0) return v.x;
@@ -473,6 +504,7 @@ struct Carry {
   f32x4 n4[RF];        // chain starts of the current group
   uint32_t sc[CF];     // binary16 scales of the current group, one per column fragment
   uint32_t sprev[CF];  // those of the previous group (its second-half chains)
+  uint32_t sh[CF][3];  // next odd code word shifted right by 4, 8, 12 (prepared form)
 };
 
 // One 32-k phase S of group step g (see compute_step).
@@ -529,7 +561,25 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
     if (k % PER_WORD == PER_WORD - 1) {
       const int jw = k / PER_WORD;
       // code word of the next phase (the next group's first word in phase 3)
-      nb[jw] = unpack_word<RAW>(word<(S + 1) & 3>(S < 3 ? C.raw[jw] : rawn[jw]));
+      if constexpr (RAW) {
+        nb[jw] = unpack_word<RAW>(word<(S + 1) & 3>(S < 3 ? C.raw[jw] : rawn[jw]));
+      } else if constexpr (S == 1 || S == 3) {
+        // even word now, and the shifted copies of the odd word after it
+        // (the next phase's) from the same three 64-bit shifts
+        const u32x4& src = S < 3 ? C.raw[jw] : rawn[jw];
+        const uint64_t q = ((uint64_t)(S == 1 ? src.w : src.y) << 32) | (S == 1 ? src.z : src.x);
+        uint64_t q4, q8, q12;
+        asm volatile("v_lshrrev_b64 %0, 4, %1" : "=v"(q4) : "v"(q));
+        asm volatile("v_lshrrev_b64 %0, 8, %1" : "=v"(q8) : "v"(q));
+        asm volatile("v_lshrrev_b64 %0, 12, %1" : "=v"(q12) : "v"(q));
+        nb[jw] = codes_from_shifts((uint32_t)q, (uint32_t)q4, (uint32_t)q8, (uint32_t)q12);
+        C.sh[jw][0] = (uint32_t)(q4 >> 32);
+        C.sh[jw][1] = (uint32_t)(q8 >> 32);
+        C.sh[jw][2] = (uint32_t)(q12 >> 32);
+      } else {
+        nb[jw] = codes_from_shifts(S == 0 ? C.raw[jw].y : C.raw[jw].w, C.sh[jw][0], C.sh[jw][1],
+                                   C.sh[jw][2]);
+      }
       pin(nb[jw]);
     }
     if constexpr (S < 2) issue_copies_at<IF, RAW>(cj, S * NC + k);
@@ -565,11 +615,11 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
 // Raw form: before the barrier each wave derives the chain starts of its 16
 // rows of group g + 1 (its own copies) and stores them.
 template <int IF, bool RAW>
-__device__ __forceinline__ void compute_step(const GemmParams& p, const Offsets<IF>& o, uint32_t os,
-                                             int64_t m0, int g, const Stage& cur,
+__device__ __forceinline__ void compute_step(const GemmParams& p, const Offsets<IF>& o,
+                                             int64_t m0, int64_t n0, int g, const Stage& cur,
                                              const Stage& nxt, const Stage& fut, uint16_t* sb,
                                              int wave, int lane, Carry<IF>& C) {
-  const CopyJob<IF> cj{p, o, os, m0, min(g + 2, p.G - 1), fut, sb, wave, lane};
+  const CopyJob<IF> cj{p, o, m0, min(g + 2, p.G - 1), n0, fut, sb, wave, lane};
   compute_phase<IF, RAW, 0>(cur, nxt, cj, g, wave, lane, C);
   compute_phase<IF, RAW, 1>(cur, nxt, cj, g, wave, lane, C);
   compute_phase<IF, RAW, 2>(cur, nxt, cj, g, wave, lane, C);
@@ -633,8 +683,6 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     o.b[j] = (uint32_t)(c * (p.K / 2) + hh * 16);
   }
   // element index (group 0) of the scale column this lane copies (waves 2-5)
-  const uint32_t os =
-      (uint32_t)(min<int64_t>(n0 + ((wave - 2) & 3) * 64 + lane, p.N - 1) * p.G);
 
   Carry<IF> C;
 #pragma unroll
@@ -651,8 +699,8 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   // last group, so every step issues the same copies; the surplus ones land
   // in a stage that is not read again)
   const int G = p.G;
-  issue_stage<IF, RAW>(CopyJob<IF>{p, o, os, m0, 0, S0, sSB, wave, lane});
-  issue_stage<IF, RAW>(CopyJob<IF>{p, o, os, m0, min(1, G - 1), S1, sSB, wave, lane});
+  issue_stage<IF, RAW>(CopyJob<IF>{p, o, m0, 0, n0, S0, sSB, wave, lane});
+  issue_stage<IF, RAW>(CopyJob<IF>{p, o, m0, min(1, G - 1), n0, S1, sSB, wave, lane});
   __builtin_amdgcn_s_waitcnt(TM::kWaitPrevGroup);
   if constexpr (RAW) {
     store_corrections(S0, wave, h, lr, row_corrections(S0, wave, h, lr));
@@ -663,7 +711,14 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   read_chain_starts<IF>(S0, wr, h, C.n4);
   read_a<IF>(S0, wr, 0, h, lr, C.a);
 #pragma unroll
-  for (int j = 0; j < CF; ++j) C.b[j] = unpack_word<RAW>(C.raw[j].x);
+  for (int j = 0; j < CF; ++j) {
+    C.b[j] = unpack_word<RAW>(C.raw[j].x);
+    if constexpr (!RAW) {
+      C.sh[j][0] = C.raw[j].y >> 4;
+      C.sh[j][1] = C.raw[j].y >> 8;
+      C.sh[j][2] = C.raw[j].y >> 12;
+    }
+  }
 
   if constexpr (RAW) {
     // the raw form holds more registers in its step (the chain starts it
@@ -674,7 +729,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     int cur = 0, nxt = 1, fut = 2;
 #pragma nounroll
     for (int g = 0; g < G; ++g) {
-      compute_step<IF, RAW>(p, o, os, m0, g, stage(cur), stage(nxt), stage(fut), sSB, wave,
+      compute_step<IF, RAW>(p, o, m0, n0, g, stage(cur), stage(nxt), stage(fut), sSB, wave,
                             lane, C);
       const int t = cur;
       cur = nxt;
@@ -684,11 +739,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   } else {
     int g = 0;
     for (;;) {
-      compute_step<IF, RAW>(p, o, os, m0, g, S0, S1, S2, sSB, wave, lane, C);
+      compute_step<IF, RAW>(p, o, m0, n0, g, S0, S1, S2, sSB, wave, lane, C);
       if (++g >= G) break;
-      compute_step<IF, RAW>(p, o, os, m0, g, S1, S2, S0, sSB, wave, lane, C);
+      compute_step<IF, RAW>(p, o, m0, n0, g, S1, S2, S0, sSB, wave, lane, C);
       if (++g >= G) break;
-      compute_step<IF, RAW>(p, o, os, m0, g, S2, S0, S1, sSB, wave, lane, C);
+      compute_step<IF, RAW>(p, o, m0, n0, g, S2, S0, S1, sSB, wave, lane, C);
       if (++g >= G) break;
     }
   }
