@@ -116,7 +116,9 @@ class ClockSampler:
         return round(sum(self.samples) / len(self.samples) / 1000.0, 3) if self.samples else None
 
 
-def build_stack(ql, synth, torch, L, d, dff):
+def build_stack(ql, synth, torch, L, d, dff, tiled=False):
+    """Packed weights of L blocks (qlinear_pack on seeded N(0, 0.02) weights),
+    each matrix's codes optionally converted to the tiled layout."""
     shapes = {"qkv": (3 * d, d), "out": (d, d), "up": (dff, d), "down": (d, dff)}
     scratch = torch.empty(dff * d, dtype=torch.float32, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -128,7 +130,8 @@ def build_stack(ql, synth, torch, L, d, dff):
             n, k = shapes[name]
             w = scratch[: n * k].view(n, k)
             synth.weights_f32_cuda(synth.matrix_seed(synth.SEED_STACK, l, i), n, k, out=w)
-            mats[name] = ql.pack(w, status=status)
+            qw, sc = ql.pack(w, status=status)
+            mats[name] = (ql.tile_codes(qw), sc, ql.LAYOUT_TILED) if tiled else (qw, sc)
         layers.append(mats)
         if l % 16 == 15:
             torch.cuda.synchronize()
@@ -143,12 +146,12 @@ def build_stack(ql, synth, torch, L, d, dff):
 def bench_stack(args, ql, synth, torch):
     d, dff, M, L = 12288, 49152, 4096, args.layers
     pairs = M // TOKENS_PER_PAIR
-    layers = build_stack(ql, synth, torch, L, d, dff)
+    layers = build_stack(ql, synth, torch, L, d, dff, tiled=args.layout == "tiled")
     arr = ql.make_layers(layers)
     ws = torch.empty(ql.stack_workspace_bytes(M, d, dff), dtype=torch.uint8, device="cuda")
     h0 = torch.from_numpy(synth.residual_f32(synth.SEED_STACK, M, d)).cuda()
     h = torch.empty_like(h0)
-    resident = sum(q.numel() + 2 * s.numel() for m in layers for q, s in m.values())
+    resident = sum(q.numel() + 2 * s.numel() for m in layers for q, s, *_ in m.values())
 
     def step(events=None):
         h.copy_(h0)          # this batch's input residual stream
@@ -211,7 +214,8 @@ def bench_stack(args, ql, synth, torch):
                                "down 49152->12288), group 128, fp16 scales, bf16 activations, "
                                "M = 4096 tokens (8 protein-ligand pairs x 512)",
                    "layers": L, "d": d, "d_ff": dff, "tokens": M, "pairs": pairs,
-                   "group": 128, "resident_weight_bytes": int(resident)},
+                   "group": 128, "resident_weight_bytes": int(resident),
+                   "weight_layout": args.layout},
         "roofline": {"bound": "mfma", "kernel": sym,
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
@@ -378,8 +382,8 @@ def bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d, dff, pairs
     the 96 blocks' bytes crosses PCIe in every step."""
     pool = []
     for l in range(min(STREAM_POOL, L)):
-        pool.append({k: (q.cpu().pin_memory(), s.cpu().pin_memory())
-                     for k, (q, s) in layers[l].items()})
+        pool.append({k: (q.cpu().pin_memory(), s.cpu().pin_memory(), *lay)
+                     for k, (q, s, *lay) in layers[l].items()})
     host_arr = ql.make_layers([pool[l % len(pool)] for l in range(L)])
     slot = ql.stack_slot_bytes(d, dff)
     slots = torch.empty(2 * slot, dtype=torch.uint8, device="cuda")
@@ -398,7 +402,7 @@ def bench_stack_streamed(args, ql, torch, layers, h, h0, ws, L, M, d, dff, pairs
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
     # the copy alone: one block's eight arrays host -> slot, back to back
-    blk = sum(q.numel() + 2 * s.numel() for q, s in pool[0].values())
+    blk = sum(q.numel() + 2 * s.numel() for q, s, *_ in pool[0].values())
     flat = torch.empty(blk, dtype=torch.uint8).pin_memory()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(cs):
@@ -512,39 +516,53 @@ def bench_ceilings(torch, reps=10):
                             "frac_hbm_peak": round(2 * n / t / 1e9 / PEAK_HBM_GBS, 4)}}
 
 
-def bench_small_batch(ql, synth, torch, reps=50, copies=4):
+def bench_small_batch(ql, synth, torch, reps=50, copies=4, tiled=True):
     """M = 8, K = 12288, N = 49152; `copies` weight copies rotated so the
     working set (1.25 GB) exceeds the 256 MB last-level cache; the median of
-    three timed loops of `reps` launches."""
+    three timed loops of `reps` launches, on the codes in the tiled layout
+    (as resident in the stack) and, for reference, in the row-major packed
+    format."""
     M, K, N = 8, 12288, 49152
     w = torch.empty((N, K), dtype=torch.float32, device="cuda")
     mats = []
     for c in range(copies):
         synth.weights_f32_cuda(synth.matrix_seed(synth.SEED_GEMV, 0, c), N, K, out=w)
-        mats.append(ql.pack(w))
+        qw, sc = ql.pack(w)
+        mats.append((qw, ql.tile_codes(qw), sc))
     del w
     x = torch.from_numpy(synth.activations_bf16(synth.SEED_GEMV, M, K).view("int16")).cuda()
     y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    # warm-up long enough for the clocks to reach their steady state under
-    # this memory-bound loop (about 20 ms of it; after 50 launches the timed
-    # loops still ran ~8 % slow), then the median of three timed loops
-    for i in range(400):
-        ql.forward(x, *mats[i % copies], out=y)
-    times = []
-    for _ in range(3):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record()
-        for i in range(reps):
-            ql.forward(x, *mats[i % copies], out=y)
-        e1.record()
-        torch.cuda.synchronize()
-        times.append(e0.elapsed_time(e1) / reps * 1e-3)
-    t = sorted(times)[1]
+
+    def run(i, tl):
+        q_rows, q_tiled, sc = mats[i % copies]
+        ql.forward_ex(x, q_tiled if tl else q_rows, sc, y, ql.EPI_NONE, None, tiled=tl)
+
+    def timed(tl):
+        # warm-up long enough for the clocks to reach their steady state under
+        # this memory-bound loop (about 20 ms of it; after 50 launches the
+        # timed loops still ran ~8 % slow), then the median of three loops
+        for i in range(400):
+            run(i, tl)
+        times = []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for i in range(reps):
+                run(i, tl)
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / reps * 1e-3)
+        return sorted(times)[1]
+
+    t_rows = timed(False)
+    t = timed(True) if tiled else t_rows
     wb = N * K // 2 + N * (K // 128) * 2
-    return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0, 2, 6, true, 4>", "avg_us": round(t * 1e6, 2),
+    return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0, 2, 6, true, 4>",
+            "weight_layout": "tiled" if tiled else "rows", "avg_us": round(t * 1e6, 2),
             "weight_GBps": round(wb / t / 1e9, 1),
             "frac_hbm_peak": round(wb / t / 1e9 / PEAK_HBM_GBS, 4),
+            "rows_layout_avg_us": round(t_rows * 1e6, 2),
             "algorithmic_bytes": int(wb + 2 * M * K + 2 * M * N),
             "traffic": measured_traffic("k_gemv<0, 2, 6, true, 4>"), "traffic_unit": "bytes/launch"}
 
@@ -645,6 +663,9 @@ def main():
                     help="skip the stack at other batch sizes")
     ap.add_argument("--no-streamed", action="store_true",
                     help="skip the variant with the weights streamed from host memory")
+    ap.add_argument("--layout", choices=("tiled", "rows"), default="tiled",
+                    help="storage order of the resident codes: the library's tiled layout "
+                         "(converted once after packing) or the row-major packed format")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
@@ -663,7 +684,7 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_extras:
         log("[bench] small-batch projection")
-        out["small_batch"] = bench_small_batch(ql, synth, torch)
+        out["small_batch"] = bench_small_batch(ql, synth, torch, tiled=args.layout == "tiled")
         log("[bench] prefill projections")
         out["prefill"] = bench_prefill(ql, synth, torch)
         log("[bench] attention kernel")

@@ -55,7 +55,7 @@ typedef struct ihipStream_t* ql_stream_t;
 enum ql_status {
     QL_OK = 0,
     QL_ERR_ARG = 1,          /* null pointer, non-positive size, K % 128 != 0  */
-    QL_ERR_UNSUPPORTED = 2,  /* group != 128, or an unknown epilogue           */
+    QL_ERR_UNSUPPORTED = 2,  /* group != 128, unknown epilogue or code layout  */
     QL_ERR_ALIGN = 3,        /* a pointer or row stride breaks 16 B alignment  */
     QL_ERR_HIP = 4,          /* a HIP runtime call or a launch failed          */
     QL_ERR_RANGE = 5,        /* pack: non-finite weight or fp16 scale overflow */
@@ -66,7 +66,29 @@ enum ql_status {
 enum ql_epilogue {
     QL_EPI_NONE = 0,         /* out (bf16)  = acc                              */
     QL_EPI_GELU = 1,         /* out (bf16)  = gelu_erf(acc)                    */
-    QL_EPI_RESID_F32 = 2     /* out (fp32) += acc   (residual stream update)   */
+    QL_EPI_RESID_F32 = 2,    /* out (fp32) += acc   (residual stream update)   */
+    QL_EPI_WEIGHTS_TILED = 0x100  /* flag OR-ed into qlinear_forward_ex's
+                                     epilogue: qweight is in QL_LAYOUT_TILED   */
+};
+
+/*
+ * Code layouts of a packed matrix's qweight (the scales are [N][K/g] in
+ * both).  QL_LAYOUT_ROWS is the packed format above, the one qlinear_pack
+ * writes, qlinear_dequant reads and every entry point accepts.
+ * QL_LAYOUT_TILED is a permutation of the same N*K/2 bytes (N % 16 == 0)
+ * for the forward paths: the 64 bytes of group j of the 16 columns
+ * 16b .. 16b+15 are one contiguous kilobyte, so that the small-batch kernel
+ * streams whole kilobytes instead of 64-byte pieces of 16 rows.  Byte
+ * 16*hh + i (hh < 4, i < 16) of column n's group j, i.e. qweight
+ * [n][64*j + 16*hh + i] in QL_LAYOUT_ROWS, sits at tiled byte
+ *     16 * (64 * ((n / 16) * (K / 128) + j) + 16 * hh + n % 16) + i.
+ * qlinear_tile_codes / qlinear_untile_codes convert; the layout is
+ * private to this library's kernels (export to other code in
+ * QL_LAYOUT_ROWS).
+ */
+enum ql_layout {
+    QL_LAYOUT_ROWS = 0,
+    QL_LAYOUT_TILED = 1
 };
 
 /* Human-readable name of a status code (static storage, never NULL). */
@@ -97,6 +119,19 @@ int qlinear_dequant(const uint8_t* qweight, const uint16_t* scales, float* w,
                     int64_t N, int64_t K, int32_t group, ql_stream_t stream);
 
 /*
+ * qlinear_tile_codes / qlinear_untile_codes -- QL_LAYOUT_ROWS codes
+ * [N][K/2] to QL_LAYOUT_TILED and back (a byte permutation; scales are not
+ * touched).  N % 16 == 0 and K % 128 == 0 (QL_ERR_ARG); both buffers
+ * N*K/2 bytes, 16-byte aligned (QL_ERR_ALIGN) and not overlapping
+ * (QL_ERR_ARG).  Not part of the paper's computation: a storage order for
+ * the forward kernels (see QL_LAYOUT_TILED).
+ */
+int qlinear_tile_codes(const uint8_t* qweight, uint8_t* tiled, int64_t N,
+                       int64_t K, ql_stream_t stream);
+int qlinear_untile_codes(const uint8_t* tiled, uint8_t* qweight, int64_t N,
+                         int64_t K, ql_stream_t stream);
+
+/*
  * qlinear_forward -- out[M][N] = bf16(x[M][K] * W_dq^T), the quantized
  * linear projection of Sec. 3.3's "batch molecular encoding" forward pass.
  * M <= 16 runs the bandwidth-bound small-batch kernel, larger M the
@@ -111,6 +146,7 @@ int qlinear_forward(const uint16_t* x, const uint8_t* qweight,
                     const uint16_t* scales, uint16_t* out,
                     int64_t M, int64_t N, int64_t K, int32_t group,
                     ql_stream_t stream);
+/* (qweight in QL_LAYOUT_ROWS; qlinear_forward_ex takes either layout) */
 
 /* Bytes of the optional workspace of qlinear_forward_ex for an M x K input
  * (0 when the small-batch kernel serves the shape). */
@@ -130,6 +166,8 @@ size_t qlinear_workspace_bytes(int64_t M, int64_t K, int32_t group);
  *              in the kernel's operand layout with its per-group sums; used
  *              only while the enqueued work runs; calls that overlap on one
  *              workspace race.
+ *   epilogue   a ql_epilogue value, | QL_EPI_WEIGHTS_TILED when qweight is
+ *              in QL_LAYOUT_TILED (then N % 16 == 0, QL_ERR_ARG otherwise).
  */
 int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
                        const uint16_t* scales, void* out, int64_t ldo,
@@ -137,10 +175,12 @@ int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
                        int32_t epilogue, void* workspace, size_t ws_bytes,
                        ql_stream_t stream);
 
-/* One packed weight matrix (device pointers). */
+/* One packed weight matrix (device pointers); layout is a ql_layout value
+ * (another value: QL_ERR_UNSUPPORTED). */
 typedef struct {
     const uint8_t* qweight;
     const uint16_t* scales;
+    int32_t layout;
 } ql_qmat;
 
 /*

@@ -21,12 +21,15 @@ __all__ = [
     "stack_workspace_bytes", "stack_workspace_offsets", "stack_forward",
     "stack_forward_timed", "make_layers", "attention", "attention_varlen",
     "stack_slot_bytes", "stack_forward_streamed", "stack_forward_noalloc",
-    "stack_scratch_capacity",
+    "stack_scratch_capacity", "LAYOUT_ROWS", "LAYOUT_TILED", "EPI_WEIGHTS_TILED",
+    "tile_codes", "untile_codes",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqlinear.so")
 GROUP = 128
 EPI_NONE, EPI_GELU, EPI_RESID_F32 = 0, 1, 2
+EPI_WEIGHTS_TILED = 0x100          # flag: qweight in LAYOUT_TILED (forward_ex)
+LAYOUT_ROWS, LAYOUT_TILED = 0, 1   # ql_layout
 
 
 class QLError(RuntimeError):
@@ -46,6 +49,8 @@ def _load():
         "qlinear_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "qlinear_pack": (ctypes.c_int, [vp, vp, vp, i64, i64, i32, vp, vp]),
         "qlinear_dequant": (ctypes.c_int, [vp, vp, vp, i64, i64, i32, vp]),
+        "qlinear_tile_codes": (ctypes.c_int, [vp, vp, i64, i64, vp]),
+        "qlinear_untile_codes": (ctypes.c_int, [vp, vp, i64, i64, vp]),
         "qlinear_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, i64, i64, i32, vp]),
         "qlinear_workspace_bytes": (sz, [i64, i64, i32]),
         "qlinear_forward_ex": (ctypes.c_int, [vp, i64, vp, vp, vp, i64, i64, i64, i64, i32,
@@ -137,9 +142,13 @@ def _attn_cfg(attn):
                                    cu.data_ptr()))
 
 
+class _QMat(ctypes.Structure):
+    _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("layout", ctypes.c_int32)]
+
+
 class _QLayer(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in (
-        "qkv_q", "qkv_s", "out_q", "out_s", "up_q", "up_s", "down_q", "down_s")]
+    _fields_ = [(n, _QMat) for n in ("qkv", "out", "up", "down")]
 
 
 # ---------------------------------------------------------------------------
@@ -164,6 +173,27 @@ def pack(w: torch.Tensor, group: int = GROUP, stream=None, check: bool = True,
         code = int(status.item())
         _check(code, "qlinear_pack (device status)")
     return qw, sc
+
+
+def tile_codes(qweight: torch.Tensor, stream=None) -> torch.Tensor:
+    """Row-major codes uint8 [N, K/2] -> the same bytes in LAYOUT_TILED order
+    (returned as a [N, K/2] uint8 tensor whose rows are not weight rows)."""
+    _need(qweight, "qweight", (torch.uint8,), 2)
+    N, H = qweight.shape
+    out = torch.empty_like(qweight, memory_format=torch.contiguous_format)
+    _check(lib.qlinear_tile_codes(_ptr(qweight.contiguous()), _ptr(out), N, 2 * H,
+                                  _stream(stream)), "qlinear_tile_codes")
+    return out
+
+
+def untile_codes(tiled: torch.Tensor, stream=None) -> torch.Tensor:
+    """Inverse of tile_codes: LAYOUT_TILED bytes [N, K/2] -> row-major codes."""
+    _need(tiled, "tiled", (torch.uint8,), 2)
+    N, H = tiled.shape
+    out = torch.empty_like(tiled, memory_format=torch.contiguous_format)
+    _check(lib.qlinear_untile_codes(_ptr(tiled.contiguous()), _ptr(out), N, 2 * H,
+                                    _stream(stream)), "qlinear_untile_codes")
+    return out
 
 
 def dequant(qweight: torch.Tensor, scales: torch.Tensor, group: int = GROUP, stream=None):
@@ -198,11 +228,14 @@ def workspace_bytes(M: int, K: int, group: int = GROUP) -> int:
 
 def forward_ex(x, qweight, scales, out, epilogue: int = EPI_NONE, workspace=None,
                M=None, N=None, K=None, ldx=None, ldo=None, group: int = GROUP, stream=None,
-               x_ptr=None):
+               x_ptr=None, tiled: bool = False):
     """Strided / fused-epilogue forward with an optional caller workspace
     (uint8 tensor; None runs the MFMA kernel on x as stored).  x may be a
     strided 2-D view (row stride ldx); out is bf16 for NONE/GELU and fp32
-    (updated in place) for RESID_F32."""
+    (updated in place) for RESID_F32.  tiled: qweight holds LAYOUT_TILED
+    codes (tile_codes)."""
+    if tiled:
+        epilogue |= EPI_WEIGHTS_TILED
     M = x.shape[0] if M is None else M
     K = x.shape[1] if K is None else K
     N = qweight.shape[0] if N is None else N
@@ -282,13 +315,17 @@ def stack_workspace_offsets(M: int, d: int, d_ff: int, group: int = GROUP):
 
 def make_layers(layers):
     """layers: list of dicts {"qkv": (qw, sc), "out": ..., "up": ..., "down": ...}
-    of device tensors -> ctypes array for stack_forward (keep the tensors alive)."""
+    of device tensors, each entry optionally (qw, sc, layout) with layout
+    LAYOUT_ROWS (default) or LAYOUT_TILED -> ctypes array for stack_forward
+    (keep the tensors alive)."""
     arr = (_QLayer * len(layers))()
     for i, L in enumerate(layers):
         for name in ("qkv", "out", "up", "down"):
-            q, s = L[name]
-            setattr(arr[i], name + "_q", q.data_ptr())
-            setattr(arr[i], name + "_s", s.data_ptr())
+            q, s, *rest = L[name]
+            m = getattr(arr[i], name)
+            m.qweight = q.data_ptr()
+            m.scales = s.data_ptr()
+            m.layout = rest[0] if rest else LAYOUT_ROWS
     return arr
 
 

@@ -30,16 +30,17 @@ size_t forward_ws_bytes(int64_t M, int64_t K) {
 // kernel on the operand prepared in the workspace, or, without one, on the
 // activations as stored.  Workspace already validated.
 int run_linear(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc, void* out,
-               int64_t ldo, int64_t M, int64_t N, int64_t K, int epi, void* ws,
+               int64_t ldo, int64_t M, int64_t N, int64_t K, int epi, bool tl, void* ws,
                hipStream_t s) {
-  if (use_gemv(M, K)) return hip_status(launch_gemv(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
-  if (!ws) return hip_status(launch_gemm_raw(x, ldx, qw, sc, out, ldo, M, N, K, epi, s));
+  if (use_gemv(M, K))
+    return hip_status(launch_gemv(x, ldx, qw, sc, out, ldo, M, N, K, epi, tl, s));
+  if (!ws) return hip_status(launch_gemm_raw(x, ldx, qw, sc, out, ldo, M, N, K, epi, tl, s));
   uint16_t* xp = static_cast<uint16_t*>(ws);
   float* ns = reinterpret_cast<float*>(static_cast<char*>(ws) + xp_bytes(M, K));
   const int64_t Mp = padded_rows(M);
   hipError_t e = launch_prep(x, ldx, xp, ns, M, K, Mp, s);
   if (e != hipSuccess) return QL_ERR_HIP;
-  return hip_status(launch_gemm(xp, ns, Mp, qw, sc, out, ldo, M, N, K, epi, s));
+  return hip_status(launch_gemm(xp, ns, Mp, qw, sc, out, ldo, M, N, K, epi, tl, s));
 }
 
 // ---- stack workspace layout
@@ -139,14 +140,19 @@ int stack_setup(float* h, int64_t M, int64_t d, int64_t d_ff, int32_t group, flo
   return QL_OK;
 }
 
+// (every stack matrix has N and K multiples of 128, so either code layout
+// applies to it)
 int check_layer(const ql_layer& Ly) {
   const ql_qmat* mats[4] = {&Ly.qkv, &Ly.out, &Ly.up, &Ly.down};
   for (const ql_qmat* q : mats) {
     if (!q->qweight || !q->scales) return QL_ERR_ARG;
+    if (q->layout != QL_LAYOUT_ROWS && q->layout != QL_LAYOUT_TILED) return QL_ERR_UNSUPPORTED;
     if (!aligned16(q->qweight) || ((uintptr_t)q->scales & 1u)) return QL_ERR_ALIGN;
   }
   return QL_OK;
 }
+
+inline bool tiled(const ql_qmat& q) { return q.layout == QL_LAYOUT_TILED; }
 
 // optional timing hook: events[8l + 2j] / [8l + 2j + 1] bracket projection j
 inline hipError_t mark(const StackRun& r, int l, int j, int end) {
@@ -169,7 +175,8 @@ hipError_t run_block(const StackRun& r, const ql_layer& Ly, int l) {
   if (r.small) {
     QL_TRY(launch_rmsnorm(r.h, r.a, nullptr, M, d, 0, r.eps, false, s));
     QL_TRY(mark(r, l, 0, 0));
-    QL_TRY(launch_gemv(r.a, d, Ly.qkv.qweight, Ly.qkv.scales, r.qkv, 3 * d, M, 3 * d, d, 0, s));
+    QL_TRY(launch_gemv(r.a, d, Ly.qkv.qweight, Ly.qkv.scales, r.qkv, 3 * d, M, 3 * d, d, 0,
+                       tiled(Ly.qkv), s));
     QL_TRY(mark(r, l, 0, 1));
     const uint16_t* v = r.qkv + 2 * d;
     int64_t ldv = 3 * d;
@@ -180,14 +187,16 @@ hipError_t run_block(const StackRun& r, const ql_layer& Ly, int l) {
       ldv = d;
     }
     QL_TRY(mark(r, l, 1, 0));
-    QL_TRY(launch_gemv(v, ldv, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2, s));
+    QL_TRY(launch_gemv(v, ldv, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2, tiled(Ly.out), s));
     QL_TRY(mark(r, l, 1, 1));
     QL_TRY(launch_rmsnorm(r.h, r.a, nullptr, M, d, 0, r.eps, false, s));
     QL_TRY(mark(r, l, 2, 0));
-    QL_TRY(launch_gemv(r.a, d, Ly.up.qweight, Ly.up.scales, r.u, d_ff, M, d_ff, d, 1, s));
+    QL_TRY(launch_gemv(r.a, d, Ly.up.qweight, Ly.up.scales, r.u, d_ff, M, d_ff, d, 1, tiled(Ly.up),
+                       s));
     QL_TRY(mark(r, l, 2, 1));
     QL_TRY(mark(r, l, 3, 0));
-    QL_TRY(launch_gemv(r.u, d_ff, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2, s));
+    QL_TRY(launch_gemv(r.u, d_ff, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2,
+                       tiled(Ly.down), s));
     QL_TRY(mark(r, l, 3, 1));
   } else {
     const GemmPrep vprep{r.av, d, r.ns1, 2 * d};  // V slice -> out-projection operand
@@ -195,7 +204,7 @@ hipError_t run_block(const StackRun& r, const ql_layer& Ly, int l) {
     QL_TRY(launch_rmsnorm(r.h, r.a, r.ns0, M, d, Mp, r.eps, true, s));
     QL_TRY(mark(r, l, 0, 0));
     QL_TRY(launch_gemm(r.a, r.ns0, Mp, Ly.qkv.qweight, Ly.qkv.scales, r.qkv, 3 * d, M, 3 * d, d,
-                       0, s, at ? nullptr : &vprep));
+                       0, tiled(Ly.qkv), s, at ? nullptr : &vprep));
     QL_TRY(mark(r, l, 0, 1));
     if (at) {
       QL_TRY(launch_attention(r.qkv, 3 * d, r.u, d, M, (int)d, at->heads, at->seq_len, at->window,
@@ -203,15 +212,17 @@ hipError_t run_block(const StackRun& r, const ql_layer& Ly, int l) {
       QL_TRY(launch_prep(r.u, d, r.av, r.ns1, M, d, Mp, s));
     }
     QL_TRY(mark(r, l, 1, 0));
-    QL_TRY(launch_gemm(r.av, r.ns1, Mp, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2, s));
+    QL_TRY(launch_gemm(r.av, r.ns1, Mp, Ly.out.qweight, Ly.out.scales, r.h, d, M, d, d, 2,
+                       tiled(Ly.out), s));
     QL_TRY(mark(r, l, 1, 1));
     QL_TRY(launch_rmsnorm(r.h, r.a, r.ns0, M, d, Mp, r.eps, true, s));
     QL_TRY(mark(r, l, 2, 0));
     QL_TRY(launch_gemm(r.a, r.ns0, Mp, Ly.up.qweight, Ly.up.scales, nullptr, d_ff, M, d_ff, d, 1,
-                       s, &uprep));
+                       tiled(Ly.up), s, &uprep));
     QL_TRY(mark(r, l, 2, 1));
     QL_TRY(mark(r, l, 3, 0));
-    QL_TRY(launch_gemm(r.u, r.ns1, Mp, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2, s));
+    QL_TRY(launch_gemm(r.u, r.ns1, Mp, Ly.down.qweight, Ly.down.scales, r.h, d, M, d, d_ff, 2,
+                       tiled(Ly.down), s));
     QL_TRY(mark(r, l, 3, 1));
   }
 #undef QL_TRY
@@ -244,7 +255,7 @@ ql_layer slot_layer(char* base, const SlotLayout& S) {
   ql_qmat m[4];
   for (int i = 0; i < 4; ++i)
     m[i] = ql_qmat{reinterpret_cast<const uint8_t*>(base + S.q[i]),
-                   reinterpret_cast<const uint16_t*>(base + S.sc[i])};
+                   reinterpret_cast<const uint16_t*>(base + S.sc[i]), QL_LAYOUT_ROWS};
   return ql_layer{m[0], m[1], m[2], m[3]};
 }
 
@@ -283,7 +294,8 @@ const char* qlinear_status_string(int status) {
   switch (status) {
     case QL_OK: return "ok";
     case QL_ERR_ARG: return "invalid argument (null pointer, non-positive size or K % 128 != 0)";
-    case QL_ERR_UNSUPPORTED: return "unsupported (group size other than 128, or unknown epilogue)";
+    case QL_ERR_UNSUPPORTED:
+      return "unsupported (group size other than 128, unknown epilogue or code layout)";
     case QL_ERR_ALIGN: return "misaligned pointer or row stride (16-byte alignment required)";
     case QL_ERR_HIP: return "HIP runtime error or launch failure";
     case QL_ERR_RANGE: return "non-finite weight or fp16 scale overflow";
@@ -312,6 +324,27 @@ int qlinear_dequant(const uint8_t* qweight, const uint16_t* scales, float* w, in
   return hip_status(launch_dequant(qweight, scales, w, N, K, (hipStream_t)stream));
 }
 
+static int tile_common(const uint8_t* src, uint8_t* dst, int64_t N, int64_t K, bool to_tiled,
+                       hipStream_t s) {
+  if (!src || !dst) return QL_ERR_ARG;
+  int rc = check_shape(1, N, K, kGroup);
+  if (rc) return rc;
+  if (N % 16) return QL_ERR_ARG;
+  if (!aligned16(src) || !aligned16(dst)) return QL_ERR_ALIGN;
+  if (overlap(src, (size_t)N * K / 2, dst, (size_t)N * K / 2)) return QL_ERR_ARG;
+  return hip_status(launch_tile_codes(src, dst, N, K, to_tiled, s));
+}
+
+int qlinear_tile_codes(const uint8_t* qweight, uint8_t* tiled, int64_t N, int64_t K,
+                       ql_stream_t stream) {
+  return tile_common(qweight, tiled, N, K, true, (hipStream_t)stream);
+}
+
+int qlinear_untile_codes(const uint8_t* tiled, uint8_t* qweight, int64_t N, int64_t K,
+                         ql_stream_t stream) {
+  return tile_common(tiled, qweight, N, K, false, (hipStream_t)stream);
+}
+
 size_t qlinear_workspace_bytes(int64_t M, int64_t K, int32_t group) {
   if (check_shape(M, 1, K, group)) return 0;
   return forward_ws_bytes(M, K);
@@ -324,8 +357,11 @@ int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
   if (!x || !qweight || !scales || !out) return QL_ERR_ARG;
   int rc = check_shape(M, N, K, group);
   if (rc) return rc;
+  const bool tl = (epilogue & QL_EPI_WEIGHTS_TILED) != 0;
+  epilogue &= ~QL_EPI_WEIGHTS_TILED;
   if (epilogue < QL_EPI_NONE || epilogue > QL_EPI_RESID_F32) return QL_ERR_UNSUPPORTED;
   if (ldx < K || ldo < N) return QL_ERR_ARG;
+  if (tl && N % 16) return QL_ERR_ARG;
   const uintptr_t esize = epilogue == QL_EPI_RESID_F32 ? 4 : 2;
   if (!aligned16(x) || !aligned16(qweight) || ((uintptr_t)out & (esize - 1)) ||
       ((uintptr_t)scales & 1u))
@@ -338,7 +374,7 @@ int qlinear_forward_ex(const uint16_t* x, int64_t ldx, const uint8_t* qweight,
     if (ws_bytes < need) return QL_ERR_WORKSPACE;
     if (!aligned256(workspace)) return QL_ERR_ALIGN;
   }
-  return run_linear(x, ldx, qweight, scales, out, ldo, M, N, K, epilogue, workspace,
+  return run_linear(x, ldx, qweight, scales, out, ldo, M, N, K, epilogue, tl, workspace,
                     (hipStream_t)stream);
 }
 
@@ -350,7 +386,7 @@ int qlinear_forward(const uint16_t* x, const uint8_t* qweight, const uint16_t* s
   if (rc) return rc;
   if (!aligned16(x) || !aligned16(qweight) || ((uintptr_t)out & 1u) || ((uintptr_t)scales & 1u))
     return QL_ERR_ALIGN;
-  return run_linear(x, K, qweight, scales, out, N, M, N, K, QL_EPI_NONE, nullptr,
+  return run_linear(x, K, qweight, scales, out, N, M, N, K, QL_EPI_NONE, false, nullptr,
                     (hipStream_t)stream);
 }
 
@@ -461,6 +497,7 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
                               &host_layers[l].down};
     for (const ql_qmat* q : mats) {
       if (!q->qweight || !q->scales) return QL_ERR_ARG;
+      if (q->layout != QL_LAYOUT_ROWS && q->layout != QL_LAYOUT_TILED) return QL_ERR_UNSUPPORTED;
       if (!pinned_host(q->qweight) || !pinned_host(q->scales)) return QL_ERR_ARG;
     }
   }
@@ -498,7 +535,12 @@ int qlayer_stack_forward_streamed(const ql_layer* host_layers, int32_t n_layers,
       if (copy_layer(l + 1, nk) != hipSuccess) { out = QL_ERR_HIP; break; }
     }
     if (hipStreamWaitEvent(s, copied[k], 0) != hipSuccess) { out = QL_ERR_HIP; break; }
-    if (run_block(r, dev[k], l) != hipSuccess) { out = QL_ERR_HIP; break; }
+    ql_layer Ly = dev[k];  // the slot's copies keep the host matrices' layouts
+    Ly.qkv.layout = host_layers[l].qkv.layout;
+    Ly.out.layout = host_layers[l].out.layout;
+    Ly.up.layout = host_layers[l].up.layout;
+    Ly.down.layout = host_layers[l].down.layout;
+    if (run_block(r, Ly, l) != hipSuccess) { out = QL_ERR_HIP; break; }
     if (hipEventRecord(freed[k], s) != hipSuccess) { out = QL_ERR_HIP; break; }
   }
   // events may be destroyed while work that records them is still queued:

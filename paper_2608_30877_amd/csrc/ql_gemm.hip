@@ -6,8 +6,10 @@
 // waves form a 2 x 4 grid, so each owns a 64 x 64 slice.  The K loop walks
 // one 128-wide scale group per step:
 //   * the activation tile (128 rows x 128 k, bf16), the packed weight tile
-//     (256 columns x 64 bytes), the group's 256 scales and 128 correction
-//     terms are copied global -> LDS with direct-to-LDS loads into a
+//     (256 columns x 64 bytes; from row-major codes 16 rows x 64 bytes per
+//     copy instruction, from the tiled layout one contiguous kilobyte), the
+//     group's 256 scales and 128 correction terms are copied global -> LDS
+//     with direct-to-LDS loads into a
 //     three-stage ring: while group g is computed, the copies of groups g+1
 //     and g+2 are in flight, so each copy has about two steps to land;
 //   * a step runs four 32-k phases; in each, a wave reads its activation
@@ -76,6 +78,7 @@ struct GemmParams {
   const uint16_t* sc;
   void* out;  // may be null when only the prepared copy is wanted
   int64_t ldo, Mp, ldx;
+  int64_t qgs;  // bytes from one group's codes to the next: 64 (row-major) or 1024 (tiled)
   int M, N, K, G;
   int tiles_m, tiles_n;
   // prepared copy of output columns >= pcol0 (see GemmPrep)
@@ -267,7 +270,7 @@ __device__ __forceinline__ void issue_copy(const CopyJob<IF>& c) {
     copy16_to_lds(xa, c.o.a[J - 1],
                   (uint32_t)reinterpret_cast<uintptr_t>(c.st.A + a_block<IF, RAW>(J - 1, wave) * 64));
   } else {
-    const char* qb = reinterpret_cast<const char*>(c.p.qw) + (size_t)c.g * (kGroup / 2);
+    const char* qb = reinterpret_cast<const char*>(c.p.qw) + (size_t)c.g * c.p.qgs;
     copy16_to_lds(qb, c.o.b[J - NA - 1],
                   (uint32_t)reinterpret_cast<uintptr_t>(c.st.B + ((J - NA - 1) * NW + wave) * 64));
   }
@@ -680,7 +683,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     const int col = slot >> 2;
     const int hh = (slot & 3) ^ b_swz(col);
     const int64_t c = min<int64_t>(n0 + col, p.N - 1);
-    o.b[j] = (uint32_t)(c * (p.K / 2) + hh * 16);
+    // row-major: column c's 64 bytes of a group at c K/2; tiled: piece hh of
+    // column c at 16 (64 (c/16) G + 16 hh + c%16) (one contiguous kilobyte
+    // per 16 columns and group, so a copy reads 1 KB in one piece)
+    o.b[j] = p.qgs == kGroup / 2 ? (uint32_t)(c * (p.K / 2) + hh * 16)
+                                 : (uint32_t)(((c >> 4) * p.G * 64 + hh * 16 + (c & 15)) * 16);
   }
   // element index (group 0) of the scale column this lane copies (waves 2-5)
 
@@ -781,11 +788,12 @@ hipError_t launch_one(const GemmParams& p, int64_t M, hipStream_t s) {
 GemmParams chunk_params(const uint16_t* x, int64_t ldx, const float* ns, int64_t Mp,
                         const uint8_t* qw, const uint16_t* sc, void* out, int64_t ldo,
                         int64_t m_s, int64_t n_s, int64_t mrows, int64_t ncols, int64_t M,
-                        int64_t N, int64_t K, size_t esize) {
+                        int64_t N, int64_t K, size_t esize, bool tiled) {
   GemmParams p;
   p.xp = x + m_s * ldx;
   p.ns = ns ? ns + m_s : nullptr;
-  p.qw = qw + n_s * (K / 2);
+  p.qw = qw + n_s * (K / 2);   // both layouts: n_s is a multiple of 16 columns
+  p.qgs = tiled ? 1024 : kGroup / 2;
   p.sc = sc + n_s * (K / kGroup);
   p.out = out ? static_cast<char*>(out) + (size_t)(m_s * ldo + n_s) * esize : nullptr;
   p.ldo = ldo;
@@ -811,7 +819,7 @@ GemmParams chunk_params(const uint16_t* x, int64_t ldx, const float* ns, int64_t
 // split here into row / column chunks that each stay below 2^31 bytes.
 hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
-                       int64_t K, int epilogue, hipStream_t s, const GemmPrep* prep) {
+                       int64_t K, int epilogue, bool tiled, hipStream_t s, const GemmPrep* prep) {
   const int64_t lim = (int64_t)1 << 31;
   const int64_t mrows = std::max<int64_t>(kGemmBM, (lim / (K * 2)) / kGemmBM * kGemmBM);
   const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
@@ -819,7 +827,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
   for (int64_t m_s = 0; m_s < M; m_s += mrows) {
     for (int64_t n_s = 0; n_s < N; n_s += ncols) {
       GemmParams p = chunk_params(xp, K, ns, Mp, qw, sc, out, ldo, m_s, n_s, mrows, ncols, M, N,
-                                  K, esize);
+                                  K, esize, tiled);
       p.pout = prep ? prep->out + m_s * prep->ld : nullptr;
       p.pns = prep ? prep->ns + m_s : nullptr;
       p.pld = prep ? prep->ld : 0;
@@ -846,7 +854,7 @@ hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const ui
 
 hipError_t launch_gemm_raw(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
                            void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
-                           hipStream_t s) {
+                           bool tiled, hipStream_t s) {
   const int64_t lim = (int64_t)1 << 31;
   const int64_t mrows = std::max<int64_t>(kGemmBM, (lim / (ldx * 2)) / kGemmBM * kGemmBM);
   const int64_t ncols = std::max<int64_t>(BN, (lim / (K / 2)) / BN * BN);
@@ -854,7 +862,7 @@ hipError_t launch_gemm_raw(const uint16_t* x, int64_t ldx, const uint8_t* qw, co
   for (int64_t m_s = 0; m_s < M; m_s += mrows) {
     for (int64_t n_s = 0; n_s < N; n_s += ncols) {
       const GemmParams p = chunk_params(x, ldx, nullptr, 0, qw, sc, out, ldo, m_s, n_s, mrows,
-                                        ncols, M, N, K, esize);
+                                        ncols, M, N, K, esize, tiled);
       hipError_t e;
       switch (epilogue) {
         case 1: e = launch_if<1, false, 8, true>(p, s); break;

@@ -31,6 +31,10 @@ hipError_t launch_pack(const float* w, uint8_t* qw, uint16_t* sc, int64_t N, int
                        int32_t* status, hipStream_t s);
 hipError_t launch_dequant(const uint8_t* qw, const uint16_t* sc, float* w, int64_t N,
                           int64_t K, hipStream_t s);
+// codes row-major [N][K/2] -> tiled (to_tiled) or back; N % 16 == 0, src and
+// dst distinct and 16-byte aligned
+hipError_t launch_tile_codes(const uint8_t* src, uint8_t* dst, int64_t N, int64_t K,
+                             bool to_tiled, hipStream_t s);
 
 // x (bf16, row stride ldx) -> xp (k-permuted bf16 [M][K]) and
 // ns[g][m] = -136 * sum_{k in group g} x[m][k]   (fp32, row stride Mp)
@@ -57,14 +61,14 @@ struct GemmPrep {
 // is given.
 hipError_t launch_gemm(const uint16_t* xp, const float* ns, int64_t Mp, const uint8_t* qw,
                        const uint16_t* sc, void* out, int64_t ldo, int64_t M, int64_t N,
-                       int64_t K, int epilogue, hipStream_t s,
+                       int64_t K, int epilogue, bool tiled, hipStream_t s,
                        const GemmPrep* prep = nullptr);
 
 // The MFMA kernel on activations as stored (row stride ldx): it derives the
 // corrections itself and needs no staging buffer (128-row tiles).
 hipError_t launch_gemm_raw(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
                            void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
-                           hipStream_t s);
+                           bool tiled, hipStream_t s);
 
 // Small-M kernel on raw bf16 activations (M <= kSmallM).  It keeps the
 // workgroup's scales in LDS: gemv_lds_bytes(K) must stay within kGemvMaxLds
@@ -76,7 +80,7 @@ inline bool use_gemv(int64_t M, int64_t K) {
 }
 hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const uint16_t* sc,
                        void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int epilogue,
-                       hipStream_t s);
+                       bool tiled, hipStream_t s);
 
 // Causal sliding-window attention over a [Q | K | V] buffer, head dim 128.
 // Uniform batch (cu_seqlens null): M = whole sequences of seq_len tokens.

@@ -84,6 +84,35 @@ hipError_t launch_dequant(const uint8_t* qw, const uint16_t* sc, float* w, int64
 }
 
 // ---------------------------------------------------------------------------
+// Code layouts: row-major [N][K/2] <-> tiled, a permutation of 16-byte
+// pieces.  Tiled piece t = ((b G + g) 4 + hh) 16 + c holds row-major piece
+// (16 b + c) 4 G + 4 g + hh: bytes 16 hh .. 16 hh + 15 of column 16 b + c's
+// 64 bytes of group g.  Thread per piece; the tiled side is the coalesced one.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_tile(const u32x4* __restrict__ src,
+                                              u32x4* __restrict__ dst, int64_t pieces, int64_t G,
+                                              bool to_tiled) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= pieces) return;
+  const int64_t b = t / (G * 64), r = t - b * (G * 64);
+  const int64_t g = r >> 6, hh = (r >> 4) & 3, c = r & 15;
+  const int64_t rm = (16 * b + c) * (4 * G) + 4 * g + hh;
+  if (to_tiled)
+    dst[t] = src[rm];
+  else
+    dst[rm] = src[t];
+}
+
+hipError_t launch_tile_codes(const uint8_t* src, uint8_t* dst, int64_t N, int64_t K,
+                             bool to_tiled, hipStream_t s) {
+  const int64_t pieces = N * K / 32;
+  hipLaunchKernelGGL(k_tile, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s,
+                     reinterpret_cast<const u32x4*>(src), reinterpret_cast<u32x4*>(dst), pieces,
+                     K / kGroup, to_tiled);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // prep: thread per 16-byte chunk (8 bf16) of x; 16 consecutive threads form
 // one 128-wide group.  Writes the k-permuted copy and the correction terms.
 // ---------------------------------------------------------------------------

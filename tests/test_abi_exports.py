@@ -33,7 +33,8 @@ def test_header_declares_the_boundary():
                  "qlayer_stack_workspace_bytes", "qlinear_rmsnorm",
                  "qlayer_stack_workspace_offsets", "qlinear_attention",
                  "qlayer_stack_forward_attn", "qlinear_attention_varlen",
-                 "qlayer_stack_forward_streamed", "qlayer_stack_slot_bytes"]:
+                 "qlayer_stack_forward_streamed", "qlayer_stack_slot_bytes",
+                 "qlinear_tile_codes", "qlinear_untile_codes"]:
         assert need in names, need
 
 
@@ -189,3 +190,68 @@ def test_streamed_stack_errors_without_launch(lib):
     # slots not 256-byte aligned
     assert f(p, 1, p, 8, 256, 1024, 128, 1e-5, None, p, big, ctypes.c_void_p(4096 + 16), big,
              s1, s2) == 3
+
+
+def test_tiled_layout_definition_matches_header_formula():
+    """tests/layout_ref.tile_np against the header's byte formula, byte by byte."""
+    import numpy as np
+    from tests.layout_ref import tile_np, untile_np
+    N, K = 48, 384
+    qw = np.random.default_rng(5).integers(0, 256, (N, K // 2), dtype=np.uint8)
+    t = tile_np(qw)
+    G = K // 128
+    for n in range(N):
+        for kb in range(K // 2):
+            j, hh, i = kb // 64, (kb % 64) // 16, kb % 16
+            assert t[16 * (64 * ((n // 16) * G + j) + 16 * hh + n % 16) + i] == qw[n, kb]
+    assert np.array_equal(untile_np(t, N, K), qw)
+
+
+def test_tile_codes_errors_without_launch(lib):
+    vp, i64 = ctypes.c_void_p, ctypes.c_int64
+    a, b = ctypes.c_void_p(1 << 20), ctypes.c_void_p(1 << 30)   # never dereferenced
+    for name in ("qlinear_tile_codes", "qlinear_untile_codes"):
+        f = getattr(lib, name)
+        f.argtypes = [vp, vp, i64, i64, vp]
+        f.restype = ctypes.c_int
+        assert f(None, b, 16, 128, None) == 1                          # null pointer
+        assert f(a, b, 24, 128, None) == 1                             # N % 16
+        assert f(a, b, 16, 100, None) == 1                             # K % 128
+        assert f(a, b, 0, 128, None) == 1                              # N <= 0
+        assert f(ctypes.c_void_p((1 << 20) + 8), b, 16, 128, None) == 3
+        assert f(a, ctypes.c_void_p((1 << 20) + 512), 16, 128, None) == 1   # overlap
+
+
+def test_tiled_flag_errors_without_launch(lib):
+    f = lib.qlinear_forward_ex
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, i64, i32, i32, vp, sz, vp]
+    f.restype = ctypes.c_int
+    p = ctypes.c_void_p(4096)
+    assert f(p, 128, p, p, p, 24, 8, 24, 128, 128, 0x100, None, 0, None) == 1   # tiled, N % 16
+    assert f(p, 128, p, p, p, 64, 8, 64, 128, 128, 0x200, None, 0, None) == 2   # unknown flag
+    assert f(p, 128, p, p, p, 64, 8, 64, 128, 128, 0x103, None, 0, None) == 2   # unknown epilogue
+
+
+def test_stack_layout_errors_without_launch(lib):
+    class QMat(ctypes.Structure):
+        _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                    ("layout", ctypes.c_int32)]
+
+    class Layer(ctypes.Structure):
+        _fields_ = [(n, QMat) for n in ("qkv", "out", "up", "down")]
+
+    f = lib.qlayer_stack_forward
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    f.argtypes = [vp, i32, vp, i64, i64, i64, i32, ctypes.c_float, vp, sz, vp]
+    f.restype = ctypes.c_int
+    p = ctypes.c_void_p(4096)
+    L = Layer()
+    for n in ("qkv", "out", "up", "down"):
+        m = getattr(L, n)
+        m.qweight, m.scales, m.layout = 1 << 20, 1 << 21, 0
+    L.up.layout = 2                                       # neither ROWS nor TILED
+    assert f(ctypes.byref(L), 1, p, 8, 256, 512, 128, 1e-5, p, 1 << 30, None) == 2
+    L.up.layout = 1
+    L.out.qweight = (1 << 20) + 8                         # misaligned codes
+    assert f(ctypes.byref(L), 1, p, 8, 256, 512, 128, 1e-5, p, 1 << 30, None) == 3
