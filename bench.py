@@ -558,13 +558,14 @@ def bench_small_batch(ql, synth, torch, reps=50, copies=4, tiled=True):
     t_rows = timed(False)
     t = timed(True) if tiled else t_rows
     wb = N * K // 2 + N * (K // 128) * 2
-    return {"shape": "M=8 K=12288 N=49152", "kernel": "k_gemv<0, 2, 6, true, 4>",
+    kern = f"k_gemv<0, 2, 6, true, 4, {'true' if tiled else 'false'}>"
+    return {"shape": "M=8 K=12288 N=49152", "kernel": kern,
             "weight_layout": "tiled" if tiled else "rows", "avg_us": round(t * 1e6, 2),
             "weight_GBps": round(wb / t / 1e9, 1),
             "frac_hbm_peak": round(wb / t / 1e9 / PEAK_HBM_GBS, 4),
             "rows_layout_avg_us": round(t_rows * 1e6, 2),
             "algorithmic_bytes": int(wb + 2 * M * K + 2 * M * N),
-            "traffic": measured_traffic("k_gemv<0, 2, 6, true, 4>"), "traffic_unit": "bytes/launch"}
+            "traffic": measured_traffic(kern), "traffic_unit": "bytes/launch"}
 
 
 def bench_prefill(ql, synth, torch, reps=10):

@@ -90,6 +90,15 @@ __device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[F], int 
       d.b[e][j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)min(g + e, G - 1) * qgs);
 }
 
+// the codes of one group (F column fragments); index clamped as in load_codes
+template <int F>
+__device__ __forceinline__ void load_group(const uint8_t* const (&wrow)[F], int g, int G,
+                                           int64_t qgs, u32x4 (&d)[F]) {
+#pragma unroll
+  for (int j = 0; j < F; ++j)
+    d[j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)min(g, G - 1) * qgs);
+}
+
 // One group: its activations (rows 4q + lane/16, chunk lane%16; L2 hits,
 // loaded here, their latency covered by the other waves of the CU) go
 // through the wave's LDS tile into the operand layout (rows past M hold stale
@@ -189,7 +198,12 @@ constexpr int gemv_wgs_per_cu() {
   return W != kWaves ? 1 : F == 3 ? 3 : 12 / F;
 }
 
-template <int EPI, int XQ, int F, bool PT, int W>
+// EARLY (pair tiles on tiled codes): each group's codes are reloaded for
+// the pair after next as soon as that group is computed, instead of both
+// after the pair; with row-major codes that splits the two 64-byte halves of
+// each 128-byte line apart (10 % slower), with tiled codes every load is a
+// whole kilobyte and the earlier requests gain 1-2 %.
+template <int EPI, int XQ, int F, bool PT, int W, bool EARLY>
 __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(GemvParams p) {
   constexpr int kCols = 16 * F;
   // [W][256 or 512] activation tiles (after the loop: [W-1][F][64] partial
@@ -271,9 +285,16 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
             for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = permute_chunk(xa[e][q]);
           load_acts(first(t + 1));
           compute_tile<F>(cb[d].b[0], xt, sS, G, g, h, lr, acc);
-          if (g + 1 < G) compute_tile<F>(cb[d].b[1], xt + 256, sS, G, g + 1, h, lr, acc);
+          if (!EARLY && g + 1 < G) compute_tile<F>(cb[d].b[1], xt + 256, sS, G, g + 1, h, lr, acc);
         }
-        load_codes(wrow, first(t + 2), G, p.qgs, cb[d]);
+        if constexpr (EARLY) {
+          load_group(wrow, first(t + 2), G, p.qgs, cb[d].b[0]);
+          if (t < TU && first(t) + 1 < G)
+            compute_tile<F>(cb[d].b[1], xt + 256, sS, G, first(t) + 1, h, lr, acc);
+          load_group(wrow, first(t + 2) + 1, G, p.qgs, cb[d].b[1]);
+        } else {
+          load_codes(wrow, first(t + 2), G, p.qgs, cb[d]);
+        }
       }
     }
   } else {
@@ -381,16 +402,19 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   // its groups, so twice the code bytes are in flight per CU
   const bool w8 = F == 3 && pt && (N + 47) / 48 <= 256 && lds_bytes<3, true, 8>(K) <= 160 * 1024;
   const int xq = (int)((M + 3) / 4);   // contiguous 4-row activation loads per group
-#define QL_GEMV(E, Q, FF, PP, WW)                                                             \
-  hipLaunchKernelGGL((k_gemv<E, Q, FF, PP, WW>),                                              \
+#define QL_GEMV(E, Q, FF, PP, WW, EE)                                                         \
+  hipLaunchKernelGGL((k_gemv<E, Q, FF, PP, WW, EE>),                                          \
                      dim3((unsigned)((N + 16 * FF - 1) / (16 * FF))), dim3(WW * 64),          \
                      (lds_bytes<FF, PP, WW>(K)), s, p)
+#define QL_GEMV_PT(E, Q, FF, WW)                        \
+  if (tiled) QL_GEMV(E, Q, FF, true, WW, true);         \
+  else QL_GEMV(E, Q, FF, true, WW, false);
 #define QL_GEMV_F(E, Q)                                 \
-  if (F == 6) QL_GEMV(E, Q, 6, true, 4);                \
-  else if (F == 3 && w8) QL_GEMV(E, Q, 3, true, 8);     \
-  else if (F == 3 && pt) QL_GEMV(E, Q, 3, true, 4);     \
-  else if (F == 3) QL_GEMV(E, Q, 3, false, 4);          \
-  else QL_GEMV(E, Q, 4, false, 4);
+  if (F == 6) { QL_GEMV_PT(E, Q, 6, 4) }                \
+  else if (F == 3 && w8) { QL_GEMV_PT(E, Q, 3, 8) }     \
+  else if (F == 3 && pt) { QL_GEMV_PT(E, Q, 3, 4) }     \
+  else if (F == 3) QL_GEMV(E, Q, 3, false, 4, false);   \
+  else QL_GEMV(E, Q, 4, false, 4, false);
 #define QL_GEMV_Q(E)                     \
   switch (xq) {                          \
     case 1: QL_GEMV_F(E, 1); break;      \
@@ -405,6 +429,7 @@ hipError_t launch_gemv(const uint16_t* x, int64_t ldx, const uint8_t* qw, const 
   }
 #undef QL_GEMV_Q
 #undef QL_GEMV_F
+#undef QL_GEMV_PT
 #undef QL_GEMV
   return hipGetLastError();
 }
