@@ -27,6 +27,56 @@ __device__ __forceinline__ float f16_to_f32(uint16_t b) {
   return (float)__builtin_bit_cast(_Float16, b);
 }
 
+// Direct-to-LDS copies: lane l writes lds + l * BYTES (a 2-byte copy writes
+// its value zero-extended into the dword lds + 4 * l).  Written as inline
+// assembly, so the compiler does not track these loads: the kernel waits for
+// them itself (s_waitcnt vmcnt), and every vector load it issues after them
+// may stay in flight while it does.  M0 carries the LDS base (one wait state
+// must separate its write from the load that reads it); M0 is a register the
+// compiler reserves, so each sequence saves and restores it instead of
+// clobbering it.  Addresses are a uniform 64-bit base in scalar registers
+// plus a per-lane 32-bit byte offset.
+#define QL_LDS_COPY(OP, V, B, L) \
+  "s_mov_b32 m0, %[" L "]\n\ts_nop 0\n\t" OP " %[" V "], %[" B "]\n\t"
+
+// one 2- or 4-byte copy
+template <int BYTES>
+__device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, const void* lds) {
+  const uint32_t l = (uint32_t)reinterpret_cast<uintptr_t>(lds);
+  uint32_t saved;
+  if constexpr (BYTES == 4) {
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dword", "o", "b", "l")
+                 "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
+  } else {
+    static_assert(BYTES == 2, "copy width");
+    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_ushort", "o", "b", "l")
+                 "s_mov_b32 m0, %[sv]"
+                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
+  }
+}
+
+// one 16-byte copy
+__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds) {
+  uint32_t saved;
+  asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dwordx4", "o", "b", "l")
+               "s_mov_b32 m0, %[sv]"
+               : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(lds) : "memory");
+}
+#undef QL_LDS_COPY
+
+// s_waitcnt immediate (gfx9 layout): vmcnt(n) (0 <= n < 64), lgkmcnt(0),
+// expcnt not waited on
+constexpr int vmcnt_lgkm0(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// also wait for every copy in flight).
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Order of the 8 k values a lane feeds to the MFMA from one 16-byte chunk.
 // The int4 unpack below yields, from one 32-bit word of 8 codes (k0 in the
 // low nibble), the pairs (k0,k4) (k1,k5) (k2,k6) (k3,k7); the activation

@@ -65,10 +65,7 @@ struct TileM {
   // group's copies are all issued, waiting until at most this many are
   // outstanding means every copy of the group before has landed.
   static constexpr int kLaterCopies = A_PER_WAVE + B_PER_WAVE;
-  static_assert(kLaterCopies < 16, "vmcnt immediate");
-  // s_waitcnt immediate (gfx9 layout): vmcnt(kLaterCopies), lgkmcnt(0),
-  // expcnt not waited on
-  static constexpr int kWaitPrevGroup = 0x0070 | kLaterCopies;
+  static constexpr int kWaitPrevGroup = vmcnt_lgkm0(kLaterCopies);
 };
 
 struct GemmParams {
@@ -121,47 +118,12 @@ __device__ __forceinline__ int a_slot(int row, int s, int h) {
 // Code tile: column n stores its 16-byte piece h at slot 4n + (h ^ b_swz(n)).
 __device__ __forceinline__ int b_swz(int col) { return ((col >> 1) ^ (col >> 2)) & 3; }
 
-// Direct-to-LDS copies: lane l writes lds + l * BYTES (a 2-byte copy writes
-// its value zero-extended into the dword lds + 4 * l).  Written as inline
-// assembly so that the compiler does not track these loads: its own wait
-// insertion cannot tell the three ring stages apart and would wait for the
-// copies just issued before every LDS read.  The kernel waits for them
-// explicitly (kWaitPrevGroup before the step barrier, vmcnt(0) before the
-// epilogue), and issues no other vector memory load in its loop.  M0 carries
-// the LDS base (one wait state must separate its write from the load that
-// reads it); M0 is a register the compiler reserves, so each sequence saves
-// and restores it instead of clobbering it.
-// Addresses are a uniform 64-bit base in scalar registers plus a per-lane
-// 32-bit byte offset, so advancing to the next group touches scalar
-// registers only.
-#define QL_LDS_COPY(OP, V, B, L) \
-  "s_mov_b32 m0, %[" L "]\n\ts_nop 0\n\t" OP " %[" V "], %[" B "]\n\t"
-
-// one 2- or 4-byte copy (correction terms, scales)
-template <int BYTES>
-__device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, const void* lds) {
-  const uint32_t l = (uint32_t)reinterpret_cast<uintptr_t>(lds);
-  uint32_t saved;
-  if constexpr (BYTES == 4) {
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dword", "o", "b", "l")
-                 "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
-  } else {
-    static_assert(BYTES == 2, "copy width");
-    asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_ushort", "o", "b", "l")
-                 "s_mov_b32 m0, %[sv]"
-                 : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(l) : "memory");
-  }
-}
-
-// one 16-byte copy (activations, codes)
-__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds) {
-  uint32_t saved;
-  asm volatile("s_mov_b32 %[sv], m0\n\t" QL_LDS_COPY("global_load_lds_dwordx4", "o", "b", "l")
-               "s_mov_b32 m0, %[sv]"
-               : [sv] "=&s"(saved) : [o] "v"(off), [b] "s"(base), [l] "s"(lds) : "memory");
-}
-#undef QL_LDS_COPY
+// The copies (copy_to_lds, copy16_to_lds: direct-to-LDS loads the compiler
+// does not track) are waited for explicitly: kWaitPrevGroup before the step
+// barrier, vmcnt(0) before the epilogue; the kernel issues no other vector
+// memory load in its loop.  Tracked copies would not do: the compiler's own
+// wait insertion cannot tell the three ring stages apart and would wait for
+// the copies just issued before every LDS read.
 
 // Anchors the computation of v at this point of the program: an empty
 // volatile statement that reads v.  The compiler otherwise moves pure
@@ -176,14 +138,6 @@ __device__ __forceinline__ void pin(const T& v) {
   } else {
     asm volatile("" ::"v"(__builtin_bit_cast(uint32_t, v)));
   }
-}
-
-// Workgroup barrier without the memory fence of __syncthreads (which would
-// also wait for every copy in flight).
-__device__ __forceinline__ void wg_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 struct Stage {

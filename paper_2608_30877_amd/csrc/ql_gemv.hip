@@ -25,8 +25,9 @@
 // from one more MFMA chain against a constant -136 operand, which starts
 // each chain so that it yields the exact code dot product.  The workgroup's
 // scales (16 F columns x G, one contiguous block of the scale matrix) are
-// copied into LDS once at the start: per-group scale loads would cost as
-// many memory instructions as the codes themselves.  The partial sums of the
+// copied into LDS once at the start, by direct-to-LDS loads issued ahead of
+// the first code loads: per-group scale loads would cost as many memory
+// instructions as the codes themselves.  The partial sums of the
 // W waves are then reduced through LDS (the wavefront reduction) and the
 // epilogue is applied.
 #include <algorithm>
@@ -254,6 +255,22 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   const int U = (G + 1) / 2;
   const int TU = U > wave ? (U - wave + W - 1) / W : 0;
   const auto first = [&](int t) { return 2 * (wave + W * t); };
+  // the workgroup's scale block goes to LDS by direct-to-LDS copies issued
+  // before the code loads, so that waiting for it (below) leaves the codes
+  // in flight (copied through registers after them, waiting for the scales
+  // had meant waiting for the first two pairs' codes too: 0.5-1.8 us); a
+  // block that is not 16-byte aligned, and the single-tile widths (whose
+  // registers are tighter), take the register copy
+  const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
+  const uint16_t* ssrc = p.sc + n0 * G;
+  const bool dma = PT && ((uintptr_t)ssrc & 15u) == 0 && (cols * G) % 8 == 0;
+  if (dma) {
+    const int nv = cols * G / 8;
+    for (int v0 = wave * 64; v0 < nv; v0 += W * 64)
+      if (v0 + lane < nv)
+        copy16_to_lds(ssrc, (uint32_t)(v0 + lane) * 16,
+                      (uint32_t)reinterpret_cast<uintptr_t>(sS + v0 * 8));
+  }
   PairCodes<F> cb[2];
   load_codes(wrow, first(0), G, p.qgs, cb[0]);
   load_codes(wrow, first(1), G, p.qgs, cb[1]);
@@ -268,9 +285,15 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
         xa[e][q] = *reinterpret_cast<const u32x4*>(xsrc[q] + (int64_t)min(g + e, G - 1) * kGroup);
   };
   if constexpr (PT) load_acts(first(0));
-  const int cols = (int)std::min<int64_t>(kCols, p.N - n0);
-  copy_scales<W>(p.sc + n0 * G, sS, cols * G);
-  __syncthreads();
+  if (dma) {
+    // the copies have landed once at most the loads issued after them are
+    // outstanding
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0(4 * F + (PT ? 2 * XQ : 0)));
+    wg_barrier();
+  } else {
+    copy_scales<W>(ssrc, sS, cols * G);
+    __syncthreads();
+  }
 
   if constexpr (PT) {
     for (int t0 = 0; t0 < TU; t0 += 2) {
