@@ -287,6 +287,38 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
     }
   }
   const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
+  if constexpr (EPI == 2) {
+    // residual update: every old value is loaded before the first store, so
+    // the loads fly together (one load after each store would wait for the
+    // store, as the compiler cannot rule out that they alias)
+    float old[RF][CF][4];
+#pragma unroll
+    for (int i = 0; i < RF; ++i)
+#pragma unroll
+      for (int j = 0; j < CF; ++j) {
+        const int64_t col = n0 + wc * (CF * 16) + j * 16 + lr;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = m0 + wr * (BM / 2) + i * 16 + h * 4 + r;
+          old[i][j][r] = col < p.N && row < p.M
+                             ? reinterpret_cast<const float*>(p.out)[row * p.ldo + col]
+                             : 0.f;
+        }
+      }
+#pragma unroll
+    for (int i = 0; i < RF; ++i)
+#pragma unroll
+      for (int j = 0; j < CF; ++j) {
+        const int64_t col = n0 + wc * (CF * 16) + j * 16 + lr;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = m0 + wr * (BM / 2) + i * 16 + h * 4 + r;
+          if (col < p.N && row < p.M)
+            reinterpret_cast<float*>(p.out)[row * p.ldo + col] = old[i][j][r] + acc[i][j][r];
+        }
+      }
+    return;
+  }
   float rs[RF][4];
 #pragma unroll
   for (int i = 0; i < RF; ++i)
@@ -302,12 +334,7 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
         const int64_t row = m0 + wr * (BM / 2) + i * 16 + h * 4 + r;
         const bool in = col < p.N && row < p.M;
         const float v = acc[i][j][r];
-        if constexpr (EPI == 2) {
-          if (in) {
-            float* o = reinterpret_cast<float*>(p.out) + row * p.ldo + col;
-            *o = *o + v;
-          }
-        } else {
+        {
           const uint16_t b = f32_to_bf16(EPI == 1 ? gelu_erf(v) : v);
           if (in && p.out) reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = b;
           if constexpr (PREP) {

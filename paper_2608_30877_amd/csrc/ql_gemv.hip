@@ -347,6 +347,30 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   for (int w = 0; w < W - 1; ++w)
 #pragma unroll
     for (int j = 0; j < F; ++j) acc[j] += red[(w * F + j) * 64 + lane];
+  if constexpr (EPI == 2) {
+    // residual update: all old values loaded before the first store (see the
+    // MFMA kernel's epilogue)
+    float old[F][4];
+#pragma unroll
+    for (int j = 0; j < F; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t col = n0 + j * 16 + lr;
+        const int row = h * 4 + r;
+        old[j][r] = col < p.N && row < p.M ? reinterpret_cast<const float*>(p.out)[row * p.ldo + col]
+                                           : 0.f;
+      }
+#pragma unroll
+    for (int j = 0; j < F; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t col = n0 + j * 16 + lr;
+        const int row = h * 4 + r;
+        if (col < p.N && row < p.M)
+          reinterpret_cast<float*>(p.out)[row * p.ldo + col] = old[j][r] + acc[j][r];
+      }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < F; ++j) {
     const int64_t col = n0 + j * 16 + lr;
@@ -356,10 +380,7 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
       const int row = h * 4 + r;
       if (row >= p.M) continue;
       const float v = acc[j][r];
-      if constexpr (EPI == 2) {
-        float* o = reinterpret_cast<float*>(p.out) + row * p.ldo + col;
-        *o = *o + v;
-      } else if constexpr (EPI == 1) {
+      if constexpr (EPI == 1) {
         reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = f32_to_bf16(gelu_erf(v));
       } else {
         reinterpret_cast<uint16_t*>(p.out)[row * p.ldo + col] = f32_to_bf16(v);
