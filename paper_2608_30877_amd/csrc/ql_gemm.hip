@@ -376,6 +376,69 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, int64_t m0, int6
   }
 }
 
+// Residual update through LDS: each half of the tile (the rows of one wave
+// row) goes into a row-major buffer T (row stride BN + 4 words: conflict-free
+// writes from the MFMA output layout), then every wave updates whole rows
+// of 256 fp32 values, one 16-byte piece per lane, so the read-modify-write
+// of the residual runs in 1 KB rows instead of 64-byte pieces of 4 rows.
+// Needs out 16-byte aligned and ldo % 4 == 0; T is the (then idle)
+// activation ring.
+template <int IF>
+__device__ __forceinline__ void store_resid_staged(const GemmParams& p, int64_t m0, int64_t n0,
+                                                   int wave, int lane,
+                                                   const f32x4 (&acc)[IF / 2][CF], float* T) {
+  constexpr int BM = TileM<IF>::BM, RF = IF / 2, HR = BM / 2, LD = BN + 4, RW = HR / NW;
+  const int h = lane >> 4, lr = lane & 15, wr = wave / WC, wc = wave % WC;
+  float* out = reinterpret_cast<float*>(p.out);
+  const int64_t col = n0 + 4 * lane;
+  const bool full = col + 3 < p.N;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+    __syncthreads();  // the ring (first half) or the previous half is no longer read
+    if (wr == hf) {
+#pragma unroll
+      for (int i = 0; i < RF; ++i)
+#pragma unroll
+        for (int j = 0; j < CF; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            T[(i * 16 + h * 4 + r) * LD + wc * (CF * 16) + j * 16 + lr] = acc[i][j][r];
+    }
+    __syncthreads();
+    f32x4 old[RW];
+#pragma unroll
+    for (int q = 0; q < RW; ++q) {
+      const int64_t row = m0 + hf * HR + wave + q * NW;
+      old[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (row < p.M) {
+        const float* o = out + row * p.ldo + col;
+        if (full) {
+          old[q] = *reinterpret_cast<const f32x4*>(o);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < p.N) old[q][e] = o[e];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < RW; ++q) {
+      const int rr = wave + q * NW;
+      const int64_t row = m0 + hf * HR + rr;
+      if (row >= p.M) continue;
+      const f32x4 v = old[q] + *reinterpret_cast<const f32x4*>(T + rr * LD + 4 * lane);
+      float* o = out + row * p.ldo + col;
+      if (full) {
+        *reinterpret_cast<f32x4*>(o) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (col + e < p.N) o[e] = v[e];
+      }
+    }
+  }
+}
+
 // activations of phase s for the wave's row fragments
 template <int IF>
 __device__ __forceinline__ void read_a(const Stage& st, int wr, int s, int h, int lr,
@@ -745,6 +808,12 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   if constexpr (PREP) {
     __shared__ float part[WC * BM];
     store_tile<EPI, true, IF>(p, m0, n0, wave, lane, C.acc, part);
+  } else if constexpr (EPI == 2) {
+    static_assert(TileM<IF>::BM / 2 * (BN + 4) * 4 <= (int)sizeof(sA), "staging buffer");
+    if (((uintptr_t)p.out & 15u) == 0 && (p.ldo & 3) == 0)
+      store_resid_staged<IF>(p, m0, n0, wave, lane, C.acc, reinterpret_cast<float*>(&sA[0][0]));
+    else
+      store_tile<EPI, false, IF>(p, m0, n0, wave, lane, C.acc, nullptr);
   } else {
     store_tile<EPI, false, IF>(p, m0, n0, wave, lane, C.acc, nullptr);
   }
