@@ -323,6 +323,30 @@ def test_forward_ex_epilogues_and_strides(ql, epi, M, with_ws):
         assert O.rel_fro(h[:, :N] - h0[:, :N], ref) <= 1e-4
 
 
+@pytest.mark.parametrize("with_ws", [False, True])
+@pytest.mark.parametrize("N,ldo", [(390, 392), (390, 393), (260, 264)])
+@pytest.mark.parametrize("M", [37, 160])
+def test_residual_epilogue_ragged_rows(ql, M, N, ldo, with_ws):
+    """fp32 residual update with a column count that ends inside a 16-byte
+    piece (N % 4 != 0) or a tile (N % 256 != 0): the MFMA kernel stages the
+    tile in LDS and updates whole rows when out and ldo allow 16-byte
+    accesses (ldo % 4 == 0), element by element otherwise (ldo = 393); the
+    columns past N stay untouched.  Without a workspace the 128-row raw
+    form runs, with one the 64- or 128-row prepared form."""
+    K = 512
+    x = synth.activations_bf16(M + N, M, K)
+    qw, sc = O.quantize_pack(synth.weights_f32(M + ldo, N, K))
+    ref = O.qlinear_ref(x, qw, sc)
+    h0 = synth.residual_f32(M + 1, M, ldo)
+    hd = dev(h0)
+    ws = (torch.empty(ql.workspace_bytes(M, K), dtype=torch.uint8, device="cuda")
+          if with_ws else None)
+    ql.forward_ex(dev_u16(x), dev(qw), dev_u16(sc), hd, ql.EPI_RESID_F32, ws, N=N, ldo=ldo)
+    h = hd.cpu().numpy()
+    np.testing.assert_array_equal(h[:, N:], h0[:, N:])
+    assert O.rel_fro(h[:, :N] - h0[:, :N], ref) <= 1e-4
+
+
 # ------------------------------------------------------------------ full-size configs
 
 def _sampled(N, n, seed):
