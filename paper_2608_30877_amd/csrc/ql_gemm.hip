@@ -555,7 +555,10 @@ struct Carry {
 };
 
 // One 32-k phase S of group step g (see compute_step).
-template <int IF, bool RAW, int S>
+// PS: consecutive code words share their shifts (64-bit shifts; see
+// codes_from_shifts), at the cost of three registers per column fragment
+// held from one phase to the next
+template <int IF, bool RAW, int S, bool PS>
 __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt,
                                               const CopyJob<IF>& cj, int g, int wave, int lane,
                                               Carry<IF>& C) {
@@ -608,7 +611,7 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
     if (k % PER_WORD == PER_WORD - 1) {
       const int jw = k / PER_WORD;
       // code word of the next phase (the next group's first word in phase 3)
-      if constexpr (RAW) {
+      if constexpr (RAW || !PS) {
         nb[jw] = unpack_word<RAW>(word<(S + 1) & 3>(S < 3 ? C.raw[jw] : rawn[jw]));
       } else if constexpr (S == 1 || S == 3) {
         // even word now, and the shifted copies of the odd word after it
@@ -661,16 +664,16 @@ __device__ __forceinline__ void compute_phase(const Stage& cur, const Stage& nxt
 // step, so every copy has about two steps to land.
 // Raw form: before the barrier each wave derives the chain starts of its 16
 // rows of group g + 1 (its own copies) and stores them.
-template <int IF, bool RAW>
+template <int IF, bool RAW, bool PS>
 __device__ __forceinline__ void compute_step(const GemmParams& p, const Offsets<IF>& o,
                                              int64_t m0, int64_t n0, int g, const Stage& cur,
                                              const Stage& nxt, const Stage& fut, uint16_t* sb,
                                              int wave, int lane, Carry<IF>& C) {
   const CopyJob<IF> cj{p, o, m0, min(g + 2, p.G - 1), n0, fut, sb, wave, lane};
-  compute_phase<IF, RAW, 0>(cur, nxt, cj, g, wave, lane, C);
-  compute_phase<IF, RAW, 1>(cur, nxt, cj, g, wave, lane, C);
-  compute_phase<IF, RAW, 2>(cur, nxt, cj, g, wave, lane, C);
-  compute_phase<IF, RAW, 3>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 0, PS>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 1, PS>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 2, PS>(cur, nxt, cj, g, wave, lane, C);
+  compute_phase<IF, RAW, 3, PS>(cur, nxt, cj, g, wave, lane, C);
 }
 
 template <int EPI, bool PREP, int IF, bool RAW>
@@ -678,6 +681,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   static_assert(!RAW || (IF == 8 && !PREP), "raw form: 128-row tiles, plain epilogues");
   using TM = TileM<IF>;
   constexpr int BM = TM::BM, RF = IF / 2;
+  // the prepared form shares the unpacking's shifts between code words,
+  // except with the plain GELU epilogue, whose loop then had no registers
+  // left for it (spilled values reloaded inside the loop, each reload
+  // waiting for every copy in flight)
+  constexpr bool PS = !RAW && !(EPI == 1 && !PREP);
   // each kind of tile of the three stages contiguous, so that one address
   // register with constant offsets reaches the same slot in every stage
   __shared__ u32x4 sA[3][TM::A_SLOTS];
@@ -764,7 +772,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
 #pragma unroll
   for (int j = 0; j < CF; ++j) {
     C.b[j] = unpack_word<RAW>(C.raw[j].x);
-    if constexpr (!RAW) {
+    if constexpr (PS) {
       C.sh[j][0] = C.raw[j].y >> 4;
       C.sh[j][1] = C.raw[j].y >> 8;
       C.sh[j][2] = C.raw[j].y >> 12;
@@ -780,7 +788,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
     int cur = 0, nxt = 1, fut = 2;
 #pragma nounroll
     for (int g = 0; g < G; ++g) {
-      compute_step<IF, RAW>(p, o, m0, n0, g, stage(cur), stage(nxt), stage(fut), sSB, wave,
+      compute_step<IF, RAW, PS>(p, o, m0, n0, g, stage(cur), stage(nxt), stage(fut), sSB, wave,
                             lane, C);
       const int t = cur;
       cur = nxt;
@@ -790,11 +798,11 @@ __global__ __launch_bounds__(NW * 64, 1) void k_gemm(GemmParams p) {
   } else {
     int g = 0;
     for (;;) {
-      compute_step<IF, RAW>(p, o, m0, n0, g, S0, S1, S2, sSB, wave, lane, C);
+      compute_step<IF, RAW, PS>(p, o, m0, n0, g, S0, S1, S2, sSB, wave, lane, C);
       if (++g >= G) break;
-      compute_step<IF, RAW>(p, o, m0, n0, g, S1, S2, S0, sSB, wave, lane, C);
+      compute_step<IF, RAW, PS>(p, o, m0, n0, g, S1, S2, S0, sSB, wave, lane, C);
       if (++g >= G) break;
-      compute_step<IF, RAW>(p, o, m0, n0, g, S2, S0, S1, sSB, wave, lane, C);
+      compute_step<IF, RAW, PS>(p, o, m0, n0, g, S2, S0, S1, sSB, wave, lane, C);
       if (++g >= G) break;
     }
   }
