@@ -41,7 +41,7 @@ which closed forms pin).  None is "parity unpinned".
 from __future__ import annotations
 
 import numpy as np
-from scipy.special import erf as _erf
+from scipy.special import erfc as _erfc
 
 __all__ = [
     "GROUP", "QMAX", "QMIN", "ERR_RANGE", "OracleRangeError",
@@ -185,9 +185,11 @@ def qlinear_ref_cols(x_bits: np.ndarray, qweight: np.ndarray, scales: np.ndarray
 
 
 def gelu(z: np.ndarray) -> np.ndarray:
-    """GELU in its exact (erf) form, fp64: z/2 (1 + erf(z / sqrt 2))."""
+    """GELU in its exact (erf) form, fp64: z/2 (1 + erf(z / sqrt 2)), evaluated
+    as z/2 erfc(-z / sqrt 2), the same function without the cancellation of
+    1 + erf for z below about -4 (relative accuracy in the negative tail)."""
     z = np.asarray(z, dtype=np.float64)
-    return 0.5 * z * (1.0 + _erf(z / np.sqrt(2.0)))
+    return 0.5 * z * _erfc(-z / np.sqrt(2.0))
 
 
 def rmsnorm_bf16(h: np.ndarray, eps: float = 1e-5) -> np.ndarray:
