@@ -347,6 +347,41 @@ def test_residual_epilogue_ragged_rows(ql, M, N, ldo, with_ws):
     assert O.rel_fro(h[:, :N] - h0[:, :N], ref) <= 1e-4
 
 
+@pytest.mark.parametrize("M,with_ws", [(8, False), (300, False), (300, True)])
+def test_gelu_epilogue_per_element(ql, M, with_ws):
+    """GELU epilogue on exact-arithmetic inputs (ternary x, uniform codes,
+    per-(column, group) power-of-two scales: every accumulator is exact),
+    element by element against the oracle's GELU of the exact product rounded
+    to bf16: at most one bf16 ulp apart, and at most 0.1 % of the elements
+    differ from the exact GELU first rounded to fp32 (the kernels' GELU is
+    an fp32 evaluation good to 7e-6 relative, tail included).  The fp32 step
+    matters for these inputs: their accumulators are multiples of 2^-6 and
+    often lie exactly halfway between two bf16 values, where GELU(z) =
+    z (1 - Q(z)) with Q below fp32's resolution of 1 rounds to the tie and
+    then to even."""
+    K, N = 1024, 4096
+    x = synth.ternary_bf16(75, M, K)
+    qw = synth.random_packed_bytes(76, N, K)
+    sc = synth.pow2_scales_f16(77, N, K // 128)
+    ws = (torch.empty(ql.workspace_bytes(M, K), dtype=torch.uint8, device="cuda")
+          if with_ws else None)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    ql.forward_ex(dev_u16(x), dev(qw), dev_u16(sc), y, ql.EPI_GELU, ws)
+    torch.cuda.synchronize()
+    acc = O.qlinear_ref(x, qw, sc)
+    g = O.gelu(acc)
+    ref = O.f64_to_bf16_bits(g).astype(np.int32)
+    ref32 = O.f64_to_bf16_bits(g.astype(np.float32).astype(np.float64)).astype(np.int32)
+    got = host_u16(y).astype(np.int32)
+    key = lambda b: np.where(b & 0x8000, -(b & 0x7FFF), b & 0x7FFF)   # ordered, +-0 equal
+    dist = np.abs(key(got) - key(ref))
+    dist32 = np.abs(key(got) - key(ref32))
+    say(f"  differing {np.mean(dist > 0):.2e} (via fp32 {np.mean(dist32 > 0):.2e}), max ulp "
+        f"{dist.max()}, negative tail (acc < -4): {np.mean(acc < -4):.3f} of the outputs")
+    assert dist.max() <= 1
+    assert np.mean(dist32 > 0) <= 1e-3
+
+
 # ------------------------------------------------------------------ full-size configs
 
 def _sampled(N, n, seed):
