@@ -138,8 +138,8 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
 // tail Q(|z|) = 1 - Phi(|z|) is evaluated as exp(-z^2/2) s P(s),
 // s = 1 / (1 + p |z|) -- the form of Abramowitz & Stegun 26.2.17, with p and
 // the seven coefficients of P (1/sqrt(2 pi) folded in) fitted for relative
-// error: at most 7e-7 in exact arithmetic and 7e-6 as evaluated here in fp32
-// over |z| <= 14 (2.3e-6 for |z| < 6), v_rcp_f32 and v_exp_f32 included.
+// error (gelu_fit.py): at most 7e-7 in exact arithmetic and about 1.2e-5
+// as evaluated here in fp32 over |z| <= 14 (3.3e-6 for |z| < 6).
 // Then Phi(z) = 1 - Q for z >= 0 and Q otherwise, so the negative tail keeps
 // its relative accuracy down to the subnormals (1 + erff(z / sqrt 2) cancels
 // in fp32 below about z = -4), at half the instructions of erff; rounded to
