@@ -6,7 +6,8 @@
 //
 // One workgroup (8 waves) owns 128 queries of one head; wave w owns 16 of
 // them.  (16 waves x 256 queries halve the key / value copies but measure
-// slower: one workgroup per CU, and 16 waves meet at every barrier.)  Key blocks of 64 keys go global -> LDS by direct-to-LDS copies into a
+// slower: one workgroup per CU, and 16 waves meet at every barrier.)  Key
+// blocks of 64 keys go global -> LDS by direct-to-LDS copies into a
 // two-stage ring (K and V both row-major, swizzled), the next block's copies
 // in flight while the current one is computed.  The scores are computed
 // transposed, S^T = K Q^T (16x16x32 bf16 MFMAs with K as the row operand), so

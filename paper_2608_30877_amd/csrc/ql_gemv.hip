@@ -9,10 +9,10 @@
 // slower).  Per group, each lane issues one 16-byte load per 16-column
 // fragment (the lane's 32 codes): 16 rows x 64 bytes from row-major codes,
 // or, from the tiled layout, one contiguous kilobyte (a pair's two loads
-// then read 2 KB in one run, 6-13 % faster); the group's activations (M rows x 256
-// bytes) come in ceil(M/4) contiguous loads of 4 rows each and reach the MFMA
-// operand layout through a wave-private LDS tile, which costs far less than
-// four 16-row loads in that layout.  With pair tiles (F = 6, and F = 3 where
+// then read 2 KB in one run, 6-13 % faster).  The group's activations
+// (M rows x 256 bytes) come in ceil(M/4) contiguous loads of 4 rows each and
+// reach the MFMA operand layout through a wave-private LDS tile, which costs
+// far less than four 16-row loads in that layout.  With pair tiles (F = 6, and F = 3 where
 // the LDS allows) each wave keeps two tiles and the next pair's activation
 // loads fly while a pair is computed; loaded just before use, their L2 round
 // trip stalled the wave once per group.  All loads are unconditional
@@ -25,9 +25,9 @@
 // from one more MFMA chain against a constant -136 operand, which starts
 // each chain so that it yields the exact code dot product.  The workgroup's
 // scales (16 F columns x G, one contiguous block of the scale matrix) are
-// copied into LDS once at the start, by direct-to-LDS loads issued ahead of
-// the first code loads: per-group scale loads would cost as many memory
-// instructions as the codes themselves.  The partial sums of the
+// copied into LDS once at the start (with pair tiles by direct-to-LDS loads
+// issued ahead of the first code loads): per-group scale loads would cost as
+// many memory instructions as the codes themselves.  The partial sums of the
 // W waves are then reduced through LDS (the wavefront reduction) and the
 // epilogue is applied.
 #include <algorithm>
