@@ -15,10 +15,12 @@
 // far less than four 16-row loads in that layout.  With pair tiles (F = 6, and F = 3 where
 // the LDS allows) each wave keeps two tiles and the next pair's activation
 // loads fly while a pair is computed; loaded just before use, their L2 round
-// trip stalled the wave once per group.  All loads are unconditional
-// (indices past the last group are clamped): the codes of two pairs stay in
-// flight in registers, and the compiler's counted waits let them fly while a
-// pair is computed.
+// trip stalled the wave once per group.  Inside the main loop every load is
+// unconditional: the codes of two pairs stay in flight in registers, and
+// the compiler's counted waits let them fly while a pair is computed.  The
+// wave's last two or three pairs run after the loop and request nothing
+// past its last pair, so that no wave waits for loads it never uses before
+// the partial sums are exchanged (that wait was 1-2 % of the kernel).
 //
 // The codes are unpacked to bf16 136 + q and run through a 16x16x32 MFMA
 // chain against the (at most 16) activation rows; the rows' group sums come
@@ -78,26 +80,60 @@ template <int F>
 struct PairCodes {
   u32x4 b[2][F];
 };
-// The pair's code loads back to back: the wave reads both 64-byte halves of
-// each 128-byte line of its 16 weight rows per fragment one right after the
-// other.  Group indices past the end are clamped (valid memory; never used).
-template <int F>
-__device__ __forceinline__ void load_codes(const uint8_t* const (&wrow)[F], int g, int G,
-                                           int64_t qgs, PairCodes<F>& d) {
-#pragma unroll
-  for (int j = 0; j < F; ++j)
-#pragma unroll
-    for (int e = 0; e < 2; ++e)
-      d.b[e][j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)min(g + e, G - 1) * qgs);
+// With pair tiles the workgroup's codes are read through one buffer
+// resource over the contiguous byte range they occupy (its columns' rows,
+// or its 16-column blocks), with that range's length as the record count:
+// a lane's address is then a 32-bit offset (half the registers of a
+// pointer, which the widest variants need to stay free of spills), and a
+// load of a group past the end (the second group of an odd G's last pair,
+// or a pair the set-up requests for a wave that has fewer) takes an offset
+// beyond that length, for which the hardware's range check returns zeros
+// without a memory access.  A range is at most 16 F x K / 2 bytes, a few
+// MB, far below kPastEnd.
+constexpr int kPastEnd = 0x40000000;
+// word 3 of a raw buffer resource: 32-bit data format, no swizzle
+constexpr int kRawBufferWord3 = 0x00020000;
+
+struct CodeSrc {
+  __amdgpu_buffer_rsrc_t rs;
+  const uint8_t* base;  // first byte of the range
+  int qgs;              // bytes from one group's codes to the next
+  int G;
+};
+
+// 16 bytes at lane offset voff of group g: through the resource (BUF: zeros
+// past the last group), or as a plain load with g clamped to the last group
+// (the single-tile widths, which run three workgroups per CU: there the
+// resource's registers pushed the loop into spills)
+template <bool BUF>
+__device__ __forceinline__ u32x4 load_code(const CodeSrc& c, uint32_t voff, int g) {
+  if constexpr (BUF) {
+    const int goff = g < c.G ? g * c.qgs : kPastEnd;
+    return __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(c.rs, (int)voff + goff, 0, 0));
+  } else {
+    return *reinterpret_cast<const u32x4*>(c.base + voff + (uint32_t)(min(g, c.G - 1) * c.qgs));
+  }
 }
 
-// the codes of one group (F column fragments); index clamped as in load_codes
-template <int F>
-__device__ __forceinline__ void load_group(const uint8_t* const (&wrow)[F], int g, int G,
-                                           int64_t qgs, u32x4 (&d)[F]) {
+// The pair's code loads back to back: the wave reads both 64-byte halves of
+// each 128-byte line of its 16 weight rows per fragment one right after the
+// other.
+template <bool BUF, int F>
+__device__ __forceinline__ void load_codes(const CodeSrc& c, const uint32_t (&voff)[F], int g,
+                                           PairCodes<F>& d) {
 #pragma unroll
   for (int j = 0; j < F; ++j)
-    d[j] = *reinterpret_cast<const u32x4*>(wrow[j] + (int64_t)min(g, G - 1) * qgs);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) d.b[e][j] = load_code<BUF>(c, voff[j], g + e);
+}
+
+// the codes of one group (F column fragments)
+template <bool BUF, int F>
+__device__ __forceinline__ void load_group(const CodeSrc& c, const uint32_t (&voff)[F], int g,
+                                           u32x4 (&d)[F]) {
+#pragma unroll
+  for (int j = 0; j < F; ++j) d[j] = load_code<BUF>(c, voff[j], g);
 }
 
 // One group: its activations (rows 4q + lane/16, chunk lane%16; L2 hits,
@@ -221,18 +257,28 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
   // rows past M and columns past N read valid (clamped) memory; their
   // results are never stored (nor are the columns whose scales the
   // workgroup's copy leaves unset)
-  const uint8_t* wrow[F];
+  const bool rows = p.qgs == kGroup / 2;
+  const int64_t lo = rows ? n0 * (p.K / 2) : n0 / 16 * G * 1024;
+  const int64_t hi = rows ? std::min<int64_t>(n0 + kCols, p.N) * (p.K / 2)
+                          : std::min<int64_t>(n0 / 16 + F, p.N / 16) * G * 1024;
+  CodeSrc cs;
+  cs.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.qw + lo), (short)0,
+                                            (int)(hi - lo), kRawBufferWord3);
+  cs.base = p.qw + lo;
+  cs.qgs = (int)p.qgs;
+  cs.G = G;
+  uint32_t voff[F];
 #pragma unroll
   for (int j = 0; j < F; ++j) {
-    if (p.qgs == kGroup / 2) {
+    if (rows) {
       // row-major: the lane's 16 bytes of its column's group
       const int64_t col = std::min<int64_t>(n0 + j * 16 + lr, p.N - 1);
-      wrow[j] = p.qw + col * (p.K / 2) + h * 16;
+      voff[j] = (uint32_t)((col - n0) * (p.K / 2) + h * 16);
     } else {
       // tiled: the fragment's 16 columns x 64 bytes of a group are one
       // contiguous kilobyte, lane l at 16 l
       const int64_t blk = std::min<int64_t>(n0 / 16 + j, p.N / 16 - 1);
-      wrow[j] = p.qw + blk * G * 1024 + lane * 16;
+      voff[j] = (uint32_t)((blk - n0 / 16) * G * 1024 + lane * 16);
     }
   }
   const uint16_t* xsrc[XQ];
@@ -272,8 +318,8 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
                       (uint32_t)reinterpret_cast<uintptr_t>(sS + v0 * 8));
   }
   PairCodes<F> cb[2];
-  load_codes(wrow, first(0), G, p.qgs, cb[0]);
-  load_codes(wrow, first(1), G, p.qgs, cb[1]);
+  load_codes<PT>(cs, voff, first(0), cb[0]);
+  load_codes<PT>(cs, voff, first(1), cb[1]);
   // pair tiles: the first pair's activations are requested before the scale
   // copy, so that their round trip overlaps it
   u32x4 xa[2][XQ];
@@ -295,45 +341,41 @@ __global__ __launch_bounds__(W * 64, (gemv_wgs_per_cu<F, W>())) void k_gemv(Gemv
     __syncthreads();
   }
 
-  if constexpr (PT) {
-    for (int t0 = 0; t0 < TU; t0 += 2) {
+  // Pair t from code buffer c.  acts: request the next pair's activations;
+  // reload: request pair t + 2 into c.  The loop runs while both pairs of
+  // an iteration have both successors, with the flags constant; the last
+  // two or three pairs follow with the flags taken per pair.
+  const auto step = [&](int t, PairCodes<F>& c, bool acts, bool reload) {
+    const int g = first(t);
+    if constexpr (PT) {
 #pragma unroll
-      for (int d = 0; d < 2; ++d) {
-        const int t = t0 + d;
-        if (t < TU) {
-          const int g = first(t);
+      for (int e = 0; e < 2; ++e)
 #pragma unroll
-          for (int e = 0; e < 2; ++e)
-#pragma unroll
-            for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = permute_chunk(xa[e][q]);
-          load_acts(first(t + 1));
-          compute_tile<F>(cb[d].b[0], xt, sS, G, g, h, lr, acc);
-          if (!EARLY && g + 1 < G) compute_tile<F>(cb[d].b[1], xt + 256, sS, G, g + 1, h, lr, acc);
-        }
-        if constexpr (EARLY) {
-          load_group(wrow, first(t + 2), G, p.qgs, cb[d].b[0]);
-          if (t < TU && first(t) + 1 < G)
-            compute_tile<F>(cb[d].b[1], xt + 256, sS, G, first(t) + 1, h, lr, acc);
-          load_group(wrow, first(t + 2) + 1, G, p.qgs, cb[d].b[1]);
-        } else {
-          load_codes(wrow, first(t + 2), G, p.qgs, cb[d]);
-        }
+        for (int q = 0; q < XQ; ++q) xt[e * 256 + xdst[q]] = permute_chunk(xa[e][q]);
+      if (acts) load_acts(first(t + 1));
+      compute_tile<F>(c.b[0], xt, sS, G, g, h, lr, acc);
+      if constexpr (EARLY) {
+        if (reload) load_group<PT>(cs, voff, first(t + 2), c.b[0]);
+        if (g + 1 < G) compute_tile<F>(c.b[1], xt + 256, sS, G, g + 1, h, lr, acc);
+        if (reload) load_group<PT>(cs, voff, first(t + 2) + 1, c.b[1]);
+      } else {
+        if (g + 1 < G) compute_tile<F>(c.b[1], xt + 256, sS, G, g + 1, h, lr, acc);
+        if (reload) load_codes<PT>(cs, voff, first(t + 2), c);
       }
+    } else {
+      compute_group<XQ, F>(c.b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
+      if (g + 1 < G) compute_group<XQ, F>(c.b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
+      if (reload) load_codes<PT>(cs, voff, first(t + 2), c);
     }
-  } else {
-    for (int t0 = 0; t0 < TU; t0 += 2) {
-#pragma unroll
-      for (int d = 0; d < 2; ++d) {
-        const int t = t0 + d;
-        if (t < TU) {
-          const int g = first(t);
-          compute_group<XQ, F>(cb[d].b[0], xsrc, xt, xdst, sS, G, g, h, lr, acc);
-          if (g + 1 < G) compute_group<XQ, F>(cb[d].b[1], xsrc, xt, xdst, sS, G, g + 1, h, lr, acc);
-        }
-        load_codes(wrow, first(t + 2), G, p.qgs, cb[d]);
-      }
-    }
+  };
+  int t0 = 0;
+  for (; t0 + 3 < TU; t0 += 2) {
+    step(t0, cb[0], true, true);
+    step(t0 + 1, cb[1], true, true);
   }
+  if (t0 < TU) step(t0, cb[0], t0 + 1 < TU, t0 + 2 < TU);
+  if (t0 + 1 < TU) step(t0 + 1, cb[1], t0 + 2 < TU, false);
+  if (t0 + 2 < TU) step(t0 + 2, cb[0], false, false);
 
   // the partial sums reuse the activation tiles' LDS
   __syncthreads();

@@ -96,6 +96,37 @@ def test_mfma_tiled_equals_rows(ql, M, N, K, epi, with_ws):
     assert torch.equal(_bits(a), _bits(b))
 
 
+# The small-batch kernel's pair loop: each wave takes every W-th pair of
+# groups, runs its main loop while two pairs ahead exist and its last two or
+# three pairs after it, requesting nothing past them; an odd G's last pair
+# has one group.  Group counts G that give every wave 0-5 pairs, with odd and
+# even counts and odd G, for the widths N selects: 6 fragments (N = 24576),
+# 3 with pair tiles (36864), 3 with eight waves (12288), 4 single tiles
+# (12304).  Exact arithmetic (ternary x, per-(column, group) power-of-two
+# scales), so both layouts must equal the oracle bit for bit on sampled
+# columns (every 5th, and the last 40).
+PAIR_TAILS = [(8, 24576, 1), (8, 24576, 3), (8, 24576, 9), (16, 24576, 17), (1, 24576, 37),
+              (8, 24576, 31), (8, 36864, 5), (13, 36864, 25), (8, 12288, 13), (4, 12288, 26),
+              (8, 12304, 3), (16, 12304, 10)]
+
+
+@pytest.mark.parametrize("M,N,G", PAIR_TAILS)
+def test_small_batch_pair_tails_exact(ql, M, N, G):
+    K = 128 * G
+    say(f"pair tails M={M} N={N} G={G}")
+    x = synth.ternary_bf16(300 + G, M, K)
+    qw = synth.random_packed_bytes(301 + G, N, K)
+    sc = synth.pow2_scales_f16(302 + G, N, G)
+    cols = np.unique(np.concatenate([np.arange(0, N, 5), np.arange(N - 40, N)]))
+    want = O.f64_to_bf16_bits(O.qlinear_ref_cols(x, qw, sc, cols))
+    qd = dev(qw)
+    for q, tiled in ((qd, False), (ql.tile_codes(qd), True)):
+        y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        ql.forward_ex(dev_u16(x), q, dev_u16(sc), y, ql.EPI_NONE, None, tiled=tiled)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host_u16(y)[:, cols], want, err_msg=f"tiled={tiled}")
+
+
 @pytest.mark.parametrize("M,N,K,with_ws", [(8, 4096, 1024, False), (300, 1296, 2048, False),
                                            (300, 1296, 2048, True)])
 def test_tiled_exact_arithmetic_against_oracle(ql, M, N, K, with_ws):
