@@ -75,14 +75,16 @@ def measured_traffic(kernel_symbol: str):
 
 
 class ClockSampler:
-    """Samples the GPU's current graphics clock (amdsmi, every ~20 ms) on a
-    host thread while the timed region runs; mean() is the average in GHz,
-    or None when the clock cannot be read."""
+    """Samples the GPU's current graphics clock and socket power (amdsmi,
+    every ~20 ms) on a host thread while the timed region runs; mean() is
+    the average clock in GHz, power() the average and largest power and the
+    power limit in W, each None when it cannot be read."""
 
     def __init__(self, interval=0.02):
         import threading
 
         self.interval, self.samples, self._stop = interval, [], threading.Event()
+        self.watts, self.limit_w = [], None
         self._thread = threading.Thread(target=self._run, daemon=True)
         try:
             import amdsmi
@@ -100,6 +102,12 @@ class ClockSampler:
                 self.samples.append(float(info["clk"]))
             except Exception:
                 pass
+            try:
+                pw = self._smi.amdsmi_get_power_info(self._h)
+                self.watts.append(float(pw["current_socket_power"]))
+                self.limit_w = float(pw["power_limit"]) / 1e6   # reported in microwatts
+            except Exception:
+                pass
             self._stop.wait(self.interval)
 
     def __enter__(self):
@@ -114,6 +122,12 @@ class ClockSampler:
 
     def mean(self):
         return round(sum(self.samples) / len(self.samples) / 1000.0, 3) if self.samples else None
+
+    def power(self):
+        if not self.watts:
+            return None
+        return {"mean_W": round(sum(self.watts) / len(self.watts), 1), "max_W": max(self.watts),
+                "limit_W": self.limit_w, "samples": len(self.watts)}
 
 
 def build_stack(ql, synth, torch, L, d, dff, tiled=False):
@@ -176,6 +190,7 @@ def bench_stack(args, ql, synth, torch):
         t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
     clock_ghz = clk.mean()
+    power = clk.power()
 
     flops = {"qkv": 2 * M * d * 3 * d, "out": 2 * M * d * d, "up": 2 * M * d * dff,
              "down": 2 * M * dff * d}
@@ -226,6 +241,9 @@ def bench_stack(args, ql, synth, torch):
                      "clock_GHz_measured": clock_ghz,
                      "frac_at_measured_clock": (round(achieved / (PEAK_BF16_TFLOPS * clock_ghz / 2.4),
                                                       4) if clock_ghz else None),
+                     # socket power over the same steps, against the board's
+                     # limit: the clock above is what that limit leaves
+                     "power_measured": power,
                      "traffic": measured_traffic(SYMBOL[sym]), "traffic_unit": "bytes/launch"},
         "kernels": kern,
         "gemm_share_of_step": round(gemm_ms / ms, 4),
