@@ -477,17 +477,24 @@ def bench_attention(ql, synth, torch, reps=20):
     heads, L, W = ATTN
     M, d = 8 * L, heads * 128
     qkv = synth.qkv_bf16_cuda(synth.SEED_STACK, M, d)
+    # two copies of the input in rotation (604 MB > the 256 MB last-level
+    # cache); untimed launches until the clock has settled, then the median
+    # of three timed loops
+    qkvs = [qkv, qkv.clone()]
     out = torch.empty((M, d), dtype=torch.bfloat16, device="cuda")
+    for i in range(10 * reps):
+        ql.attention(qkvs[i % 2], heads, L, W, out=out)
+    times = []
     for _ in range(3):
-        ql.attention(qkv, heads, L, W, out=out)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        ql.attention(qkv, heads, L, W, out=out)
-    e1.record()
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps * 1e-3
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            ql.attention(qkvs[i % 2], heads, L, W, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / reps * 1e-3)
+    t = sorted(times)[1]
     abytes = (3 * d + d) * 2 * M
     flops = 4 * heads * (M // L) * (L * (L + 1) // 2) * 128
     return {"shape": f"M={M} heads={heads} head_dim=128 seq_len={L} window={W}",
