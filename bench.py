@@ -508,33 +508,36 @@ def bench_attention(ql, synth, torch, reps=20):
 def bench_ceilings(torch, reps=10):
     """Context for the roofline fractions, measured on the same box: dense
     bf16 GEMM through torch.matmul (hipBLASLt) at the large-M projection
-    shape, and a device-to-device copy (HBM read + write)."""
+    shape, and a device-to-device copy (HBM read + write); each after
+    untimed repetitions, the median of three timed loops."""
+
+    def settled(fn):
+        for _ in range(reps):
+            fn()
+        times = []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / reps * 1e-3)
+        return sorted(times)[1]
+
     M, K, N = 4096, 12288, 49152
     g = torch.Generator("cuda").manual_seed(0)
     a = torch.randn((M, K), device="cuda", generator=g).to(torch.bfloat16)
     b = torch.randn((K, N), device="cuda", generator=g).to(torch.bfloat16)
     c = a @ b
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        torch.matmul(a, b, out=c)
-    e1.record()
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps * 1e-3
+    t = settled(lambda: torch.matmul(a, b, out=c))
     gemm_tf = 2 * M * N * K / t / 1e12
     del a, b, c
     n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps * 1e-3
+    t = settled(lambda: dst.copy_(src))
     return {"hipblaslt_bf16_dense": {"shape": f"M={M} K={K} N={N}", "tflops": round(gemm_tf, 1),
                                      "frac_bf16_peak": round(gemm_tf / PEAK_BF16_TFLOPS, 4)},
             "device_copy": {"bytes": n, "GBps_read_plus_write": round(2 * n / t / 1e9, 1),
